@@ -1,0 +1,805 @@
+// gem_api.cpp -- the libgem C ABI: device state, validation, pass planning,
+// the queuing schedule and checkpoints.  Kernels live in gem_kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/gem.h"
+#include "gem_device.hpp"
+#include "gem_internal.hpp"
+
+using gemk::PassArgs;
+using gemk::Source;
+
+struct gem_handle {
+    int device = 0;
+    int64_t P = 0;
+    int64_t Pp = 0;       // row length padded to a multiple of 64 elements (256 B)
+    int32_t n = 0;
+    gem_hyperparams hp{};
+    hipStream_t stream = nullptr;
+    float* theta = nullptr;   // [Pp]
+    float* S = nullptr;       // [n][Pp]
+    float* M = nullptr;       // [n][Pp]
+    float* h = nullptr;       // [Pp]
+    float* ts = nullptr;      // [Pp]
+    double* acc = nullptr;    // [5]: sum_ek, sum_proxy, n_clamped, n_elem_commits, loss
+    bool have_problem = false;
+    gem_sim_params sp{};
+    int64_t t = 0;
+    std::vector<int64_t> pc;  // pull clock of each worker
+    bool diag_on = false;
+    int64_t diag_commits = 0;
+    gem_stats_t stats{};
+};
+
+namespace {
+
+constexpr int64_t kRowAlign = 64;
+
+thread_local char g_last_error[512] = "";
+
+void note_hip_error(const char* what, hipError_t e, int line)
+{
+    std::snprintf(g_last_error, sizeof(g_last_error), "%s failed at gem_api.cpp:%d: %s (%d)", what,
+                  line, hipGetErrorString(e), static_cast<int>(e));
+}
+
+#define GEM_HIP(expr)                                        \
+    do {                                                     \
+        const hipError_t gem_e_ = (expr);                    \
+        if (gem_e_ != hipSuccess) {                          \
+            note_hip_error(#expr, gem_e_, __LINE__);         \
+            return GEM_EHIP;                                 \
+        }                                                    \
+    } while (0)
+
+bool valid_hp(const gem_hyperparams& hp)
+{
+    if (hp.pi_mode != GEM_PI_CLAMP0 && hp.pi_mode != GEM_PI_LITERAL) return false;
+    if (hp.kappa_mode != GEM_KAPPA_LINEAR && hp.kappa_mode != GEM_KAPPA_SQRT) return false;
+    if (hp.pull_mode != GEM_PULL_POST_COMMIT && hp.pull_mode != GEM_PULL_PRE_COMMIT) return false;
+    if (hp.rule != GEM_RULE_GEM && hp.rule != GEM_RULE_DOWNPOUR && hp.rule != GEM_RULE_ADAPTIVE)
+        return false;
+    if (!std::isfinite(hp.momentum) || !std::isfinite(hp.eps) || !std::isfinite(hp.kappa))
+        return false;
+    if (hp.kappa_mode == GEM_KAPPA_SQRT && hp.kappa < 0.0f) return false;
+    return true;
+}
+
+// kappa as it multiplies |m| (binary32, correctly rounded square root).
+float kappa_eff(const gem_hyperparams& hp)
+{
+    return hp.kappa_mode == GEM_KAPPA_SQRT ? std::sqrt(hp.kappa) : hp.kappa;
+}
+
+bool fast_rule(const gem_hyperparams& hp)
+{
+    return hp.rule == GEM_RULE_GEM && hp.pi_mode == GEM_PI_CLAMP0 &&
+           hp.pull_mode == GEM_PULL_POST_COMMIT && kappa_eff(hp) == 1.0f;
+}
+
+uint32_t mode_bits(const gem_hyperparams& hp)
+{
+    uint32_t m = 0;
+    if (hp.pi_mode == GEM_PI_LITERAL) m |= gemk::kModeLiteralPi;
+    if (kappa_eff(hp) != 1.0f) m |= gemk::kModeKappaMul;
+    if (hp.pull_mode == GEM_PULL_PRE_COMMIT) m |= gemk::kModePrePull;
+    if (hp.rule == GEM_RULE_DOWNPOUR) m |= gemk::kModeDownpour;
+    if (hp.rule == GEM_RULE_ADAPTIVE) m |= gemk::kModeAdaptive;
+    return m;
+}
+
+int64_t next_pull(const gem_handle* g, int64_t t)
+{
+    return g->hp.pull_mode == GEM_PULL_PRE_COMMIT ? t : t + 1;
+}
+
+// Check a commit sequence against the pull bookkeeping without changing it.
+int check_sequence(const gem_handle* g, const int32_t* worker, const int32_t* tau, int64_t T)
+{
+    if (T > 0 && !worker) return GEM_EINVAL;
+    if (g->t + T > static_cast<int64_t>(UINT32_MAX)) return GEM_EINVAL;  // clock keys the noise
+    std::vector<int64_t> pc = g->pc;
+    for (int64_t j = 0; j < T; ++j) {
+        const int32_t w = worker[j];
+        if (w < 0 || w >= g->n) return GEM_EWORKER;
+        const int64_t t = g->t + j;
+        if (tau && static_cast<int64_t>(tau[j]) != t - pc[w]) return GEM_ESTALE;
+        pc[w] = next_pull(g, t);
+    }
+    return GEM_OK;
+}
+
+// Routes for the first k commits of `worker`: a worker's first commit in the
+// pass reads its rows from HBM, its last writes them back; in between its
+// pair lives in one register slot.  Returns false if more than kHeldSlots
+// workers would be held at once.
+bool assign_routes(const int32_t* worker, int k, uint8_t* routes)
+{
+    int32_t slot_worker[gemk::kHeldSlots] = {};
+    bool slot_busy[gemk::kHeldSlots] = {};
+    for (int j = 0; j < k; ++j) {
+        const int32_t w = worker[j];
+        int held = -1;
+        for (int s = 0; s < gemk::kHeldSlots; ++s)
+            if (slot_busy[s] && slot_worker[s] == w) held = s;
+        bool again = false;
+        for (int q = j + 1; q < k; ++q)
+            if (worker[q] == w) { again = true; break; }
+        uint8_t src = held >= 0 ? static_cast<uint8_t>(held) : gemk::kFromHbm;
+        uint8_t dst = gemk::kToHbm;
+        if (again) {
+            int s = held;
+            if (s < 0) {
+                for (int q = 0; q < gemk::kHeldSlots && s < 0; ++q)
+                    if (!slot_busy[q]) s = q;
+                if (s < 0) return false;
+                slot_busy[s] = true;
+                slot_worker[s] = w;
+            }
+            dst = static_cast<uint8_t>(s);
+        } else if (held >= 0) {
+            slot_busy[held] = false;
+        }
+        routes[j] = gemk::route(src, dst);
+    }
+    return true;
+}
+
+struct Pass {
+    int32_t K = 0;
+    int32_t worker[GEM_K_MAX];
+    int32_t tau[GEM_K_MAX];
+    uint8_t routes[GEM_K_MAX];
+    int32_t distinct = 0;
+};
+
+// Cut a validated commit sequence into passes of at most Kmax commits.
+void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t Kmax,
+                 std::vector<Pass>& out)
+{
+    std::vector<int64_t> pc = g->pc;
+    int64_t j0 = 0;
+    while (j0 < T) {
+        Pass p;
+        int k = static_cast<int>(std::min<int64_t>(Kmax, T - j0));
+        while (k > 1 && !assign_routes(worker + j0, k, p.routes)) --k;
+        if (k == 1) assign_routes(worker + j0, 1, p.routes);
+        p.K = k;
+        for (int j = 0; j < k; ++j) {
+            const int32_t w = worker[j0 + j];
+            const int64_t t = g->t + j0 + j;
+            p.worker[j] = w;
+            p.tau[j] = static_cast<int32_t>(t - pc[w]);
+            pc[w] = next_pull(g, t);
+            bool seen = false;
+            for (int q = 0; q < j; ++q) seen = seen || (p.worker[q] == w);
+            if (!seen) p.distinct += 1;
+        }
+        out.push_back(p);
+        j0 += k;
+    }
+}
+
+void base_args(const gem_handle* g, PassArgs& a)
+{
+    std::memset(&a, 0, sizeof(a));
+    a.theta = g->theta;
+    a.S = g->S;
+    a.M = g->M;
+    a.h = g->h;
+    a.ts = g->ts;
+    a.diag = g->acc;
+    a.Pp = g->Pp;
+    a.P = g->P;
+    a.key0 = static_cast<uint32_t>(g->sp.seed);
+    a.key1 = static_cast<uint32_t>(g->sp.seed >> 32);
+    a.neg_lr = -g->sp.lr;
+    a.sigma = g->sp.sigma;
+    a.mu = g->hp.momentum;
+    a.eps = g->hp.eps;
+    a.k_eff = kappa_eff(g->hp);
+    a.mode = mode_bits(g->hp);
+}
+
+// Queue the planned passes; advance the clock and pull bookkeeping.
+int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
+               const void* const* upd, bool bf16_out)
+{
+    PassArgs a;
+    base_args(g, a);
+    const bool fast = fast_rule(g->hp);
+    int64_t j0 = 0;
+    const double row_bytes = 4.0 * static_cast<double>(g->Pp);
+    for (const Pass& p : passes) {
+        a.t0 = static_cast<uint32_t>(g->t);
+        a.K = p.K;
+        std::memcpy(a.worker, p.worker, sizeof(p.worker));
+        std::memcpy(a.tau, p.tau, sizeof(p.tau));
+        std::memcpy(a.routes, p.routes, sizeof(p.routes));
+        double bytes = 2.0 * row_bytes + 4.0 * row_bytes * p.distinct;   // theta r+w, S/M r+w
+        if (src == Source::Generated) {
+            bytes += 2.0 * row_bytes;                                     // h, theta*
+        } else {
+            for (int j = 0; j < p.K; ++j) a.upd[j] = upd[j0 + j];
+            bytes += (src == Source::GivenBF16 ? 0.5 : 1.0) * row_bytes * p.K;
+        }
+        GEM_HIP(gemk::launch_pass(a, src, fast, bf16_out, g->diag_on, g->stream));
+        for (int j = 0; j < p.K; ++j) g->pc[p.worker[j]] = next_pull(g, g->t + j);
+        g->t += p.K;
+        j0 += p.K;
+        g->stats.commits += p.K;
+        g->stats.passes += 1;
+        g->stats.alg_bytes += bytes;
+        if (g->diag_on) g->diag_commits += p.K;
+    }
+    return GEM_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* gem_last_error(void) { return g_last_error; }
+
+const char* gem_strerror(int code)
+{
+    switch (code) {
+    case GEM_OK: return "ok";
+    case GEM_EINVAL: return "invalid argument";
+    case GEM_ENOMEM: return "out of memory";
+    case GEM_EWORKER: return "worker id out of range";
+    case GEM_ESTALE: return "staleness disagrees with the pull bookkeeping";
+    case GEM_EDTYPE: return "unknown update dtype";
+    case GEM_EHIP: return "HIP runtime error";
+    case GEM_ESTATE: return "operation needs a problem set with gem_set_quadratic";
+    case GEM_EIO: return "checkpoint I/O error or mismatch";
+    case GEM_EALIGN: return "device buffer not aligned";
+    default: return "unknown error";
+    }
+}
+
+int gem_hyperparams_default(gem_hyperparams* hp)
+{
+    if (!hp) return GEM_EINVAL;
+    std::memset(hp, 0, sizeof(*hp));
+    hp->momentum = 0.9f;
+    hp->eps = 1e-16f;
+    hp->kappa = 1.0f;
+    hp->pi_mode = GEM_PI_CLAMP0;
+    hp->kappa_mode = GEM_KAPPA_LINEAR;
+    hp->pull_mode = GEM_PULL_POST_COMMIT;
+    hp->rule = GEM_RULE_GEM;
+    return GEM_OK;
+}
+
+int gem_destroy(gem_t* g)
+{
+    if (!g) return GEM_EINVAL;
+    (void)hipStreamSynchronize(g->stream);
+    (void)hipFree(g->theta);
+    (void)hipFree(g->S);
+    (void)hipFree(g->M);
+    (void)hipFree(g->h);
+    (void)hipFree(g->ts);
+    (void)hipFree(g->acc);
+    delete g;
+    return GEM_OK;
+}
+
+int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, gem_t** out)
+{
+    if (!out || P < 1 || n < 1) return GEM_EINVAL;
+    *out = nullptr;
+    gem_hyperparams h;
+    if (hp) h = *hp;
+    else gem_hyperparams_default(&h);
+    if (!valid_hp(h)) return GEM_EINVAL;
+    const int64_t Pp = (P + kRowAlign - 1) / kRowAlign * kRowAlign;
+    if (Pp / 4 > static_cast<int64_t>(UINT32_MAX) * 256) return GEM_EINVAL;
+    gem_handle* g = new (std::nothrow) gem_handle();
+    if (!g) return GEM_ENOMEM;
+    g->P = P;
+    g->Pp = Pp;
+    g->n = n;
+    g->hp = h;
+    g->pc.assign(static_cast<size_t>(n), 0);
+    {
+        const hipError_t e = hipGetDevice(&g->device);
+        if (e != hipSuccess) {
+            note_hip_error("hipGetDevice", e, __LINE__);
+            delete g;
+            return GEM_EHIP;
+        }
+    }
+    // NULL is the device's null stream, which is also torch's default stream.
+    g->stream = static_cast<hipStream_t>(stream);
+    const size_t row = static_cast<size_t>(Pp) * sizeof(float);
+    const size_t tab = row * static_cast<size_t>(n);
+    {
+        hipError_t e = hipMalloc(&g->theta, row);
+        if (e == hipSuccess) e = hipMalloc(&g->S, tab);
+        if (e == hipSuccess) e = hipMalloc(&g->M, tab);
+        if (e == hipSuccess) e = hipMalloc(&g->acc, 8 * sizeof(double));
+        if (e != hipSuccess) {
+            note_hip_error("hipMalloc", e, __LINE__);
+            (void)hipGetLastError();
+            gem_destroy(g);
+            return GEM_ENOMEM;
+        }
+    }
+    const int rc = [&]() -> int {
+        GEM_HIP(hipMemsetAsync(g->theta, 0, row, g->stream));
+        GEM_HIP(hipMemsetAsync(g->S, 0, tab, g->stream));
+        GEM_HIP(hipMemsetAsync(g->M, 0, tab, g->stream));
+        GEM_HIP(hipMemsetAsync(g->acc, 0, 8 * sizeof(double), g->stream));
+        GEM_HIP(hipStreamSynchronize(g->stream));
+        return GEM_OK;
+    }();
+    if (rc != GEM_OK) {
+        gem_destroy(g);
+        return rc;
+    }
+    *out = g;
+    return GEM_OK;
+}
+
+int gem_set_theta(gem_t* g, const float* theta0, int32_t in_is_device)
+{
+    if (!g || !theta0) return GEM_EINVAL;
+    const size_t bytes = static_cast<size_t>(g->P) * sizeof(float);
+    GEM_HIP(hipMemcpyAsync(g->theta, theta0, bytes,
+                           in_is_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
+                           g->stream));
+    GEM_HIP(gemk::launch_fill_rows(g->S, g->theta, g->Pp, g->n, g->stream));
+    GEM_HIP(hipMemsetAsync(g->M, 0, static_cast<size_t>(g->Pp) * g->n * sizeof(float), g->stream));
+    GEM_HIP(hipMemsetAsync(g->acc, 0, 8 * sizeof(double), g->stream));
+    GEM_HIP(hipStreamSynchronize(g->stream));
+    g->t = 0;
+    std::fill(g->pc.begin(), g->pc.end(), 0);
+    g->diag_commits = 0;
+    return GEM_OK;
+}
+
+int gem_set_quadratic(gem_t* g, const float* h, const float* theta_star, const gem_sim_params* sp)
+{
+    if (!g || !h || !theta_star || !sp) return GEM_EINVAL;
+    if (sp->update_dtype != GEM_F32 && sp->update_dtype != GEM_BF16) return GEM_EDTYPE;
+    if (!std::isfinite(sp->lr) || !std::isfinite(sp->sigma)) return GEM_EINVAL;
+    const size_t row = static_cast<size_t>(g->Pp) * sizeof(float);
+    if (!g->h) {
+        if (hipMalloc(&g->h, row) != hipSuccess || hipMalloc(&g->ts, row) != hipSuccess) {
+            (void)hipGetLastError();
+            (void)hipFree(g->h);
+            (void)hipFree(g->ts);
+            g->h = g->ts = nullptr;
+            return GEM_ENOMEM;
+        }
+    }
+    const size_t bytes = static_cast<size_t>(g->P) * sizeof(float);
+    GEM_HIP(hipMemsetAsync(g->h, 0, row, g->stream));
+    GEM_HIP(hipMemsetAsync(g->ts, 0, row, g->stream));
+    GEM_HIP(hipMemcpyAsync(g->h, h, bytes, hipMemcpyHostToDevice, g->stream));
+    GEM_HIP(hipMemcpyAsync(g->ts, theta_star, bytes, hipMemcpyHostToDevice, g->stream));
+    GEM_HIP(hipStreamSynchronize(g->stream));
+    g->sp = *sp;
+    g->have_problem = true;
+    return GEM_OK;
+}
+
+int gem_commit_batch(gem_t* g, int32_t K, const void* const* dthetas_dev, int32_t dtype,
+                     const int32_t* worker_ids, const int32_t* staleness)
+{
+    if (!g || K < 0 || (K > 0 && (!dthetas_dev || !worker_ids))) return GEM_EINVAL;
+    if (dtype != GEM_F32 && dtype != GEM_BF16) return GEM_EDTYPE;
+    const size_t align = dtype == GEM_F32 ? 16 : 8;
+    for (int32_t j = 0; j < K; ++j) {
+        if (!dthetas_dev[j]) return GEM_EINVAL;
+        if (!aligned(dthetas_dev[j], align)) return GEM_EALIGN;
+    }
+    int rc = check_sequence(g, worker_ids, staleness, K);
+    if (rc) return rc;
+    std::vector<Pass> passes;
+    plan_passes(g, worker_ids, K, GEM_K_MAX, passes);
+    return run_passes(g, passes, dtype == GEM_F32 ? Source::GivenF32 : Source::GivenBF16,
+                      dthetas_dev, false);
+}
+
+int gem_commit(gem_t* g, const float* dtheta_dev, int32_t worker_id)
+{
+    const void* p = dtheta_dev;
+    return gem_commit_batch(g, 1, &p, GEM_F32, &worker_id, nullptr);
+}
+
+int gem_generate(gem_t* g, int32_t worker_id, void* out_dev, int32_t dtype)
+{
+    if (!g || !out_dev) return GEM_EINVAL;
+    if (dtype != GEM_F32 && dtype != GEM_BF16) return GEM_EDTYPE;
+    if (!g->have_problem) return GEM_ESTATE;
+    if (worker_id < 0 || worker_id >= g->n) return GEM_EWORKER;
+    if (!aligned(out_dev, dtype == GEM_F32 ? 16 : 8)) return GEM_EALIGN;
+    if (g->t > static_cast<int64_t>(UINT32_MAX)) return GEM_EINVAL;
+    GEM_HIP(gemk::launch_generate(g->S + static_cast<int64_t>(worker_id) * g->Pp, g->h, g->ts,
+                                  out_dev, dtype == GEM_BF16, g->P, static_cast<uint32_t>(g->t),
+                                  static_cast<uint32_t>(g->sp.seed),
+                                  static_cast<uint32_t>(g->sp.seed >> 32), -g->sp.lr, g->sp.sigma,
+                                  g->stream));
+    return GEM_OK;
+}
+
+int gem_sim_run(gem_t* g, const int32_t* worker, const int32_t* tau, int64_t T, int32_t K)
+{
+    if (!g || T < 0 || K < 1 || K > GEM_K_MAX) return GEM_EINVAL;
+    if (!g->have_problem) return GEM_ESTATE;
+    int rc = check_sequence(g, worker, tau, T);
+    if (rc) return rc;
+    std::vector<Pass> passes;
+    plan_passes(g, worker, T, K, passes);
+    return run_passes(g, passes, Source::Generated, nullptr, g->sp.update_dtype == GEM_BF16);
+}
+
+int gem_read_theta(gem_t* g, float* out, int32_t out_is_device)
+{
+    if (!g || !out) return GEM_EINVAL;
+    GEM_HIP(hipMemcpyAsync(out, g->theta, static_cast<size_t>(g->P) * sizeof(float),
+                           out_is_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost,
+                           g->stream));
+    GEM_HIP(hipStreamSynchronize(g->stream));
+    return GEM_OK;
+}
+
+int gem_read_state(gem_t* g, int32_t w, int32_t which, float* out, int32_t out_is_device)
+{
+    if (!g || !out) return GEM_EINVAL;
+    if (w < 0 || w >= g->n) return GEM_EWORKER;
+    if (which != GEM_SNAPSHOT && which != GEM_MOMENT) return GEM_EINVAL;
+    const float* src = (which == GEM_SNAPSHOT ? g->S : g->M) + static_cast<int64_t>(w) * g->Pp;
+    GEM_HIP(hipMemcpyAsync(out, src, static_cast<size_t>(g->P) * sizeof(float),
+                           out_is_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost,
+                           g->stream));
+    GEM_HIP(hipStreamSynchronize(g->stream));
+    return GEM_OK;
+}
+
+int gem_gather(gem_t* g, const int64_t* idx, int64_t count, float* theta_out, float* S_out,
+               float* M_out)
+{
+    if (!g || count < 0 || (count > 0 && !idx)) return GEM_EINVAL;
+    if (count == 0) return GEM_OK;
+    for (int64_t k = 0; k < count; ++k)
+        if (idx[k] < 0 || idx[k] >= g->P) return GEM_EINVAL;
+    const int64_t rows = 1 + 2 * static_cast<int64_t>(g->n);
+    int64_t* d_idx = nullptr;
+    float* d_out = nullptr;
+    if (hipMalloc(&d_idx, static_cast<size_t>(count) * sizeof(int64_t)) != hipSuccess ||
+        hipMalloc(&d_out, static_cast<size_t>(count * rows) * sizeof(float)) != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFree(d_idx);
+        return GEM_ENOMEM;
+    }
+    int rc = GEM_OK;
+    do {
+        if (hipMemcpyAsync(d_idx, idx, static_cast<size_t>(count) * sizeof(int64_t),
+                           hipMemcpyHostToDevice, g->stream) != hipSuccess) { rc = GEM_EHIP; break; }
+        if (theta_out && gemk::launch_gather(g->theta, d_idx, count, d_out, g->stream) != hipSuccess) {
+            rc = GEM_EHIP;
+            break;
+        }
+        for (int32_t w = 0; w < g->n && rc == GEM_OK; ++w) {
+            if (S_out && gemk::launch_gather(g->S + static_cast<int64_t>(w) * g->Pp, d_idx, count,
+                                             d_out + (1 + w) * count, g->stream) != hipSuccess)
+                rc = GEM_EHIP;
+            if (M_out && gemk::launch_gather(g->M + static_cast<int64_t>(w) * g->Pp, d_idx, count,
+                                             d_out + (1 + g->n + w) * count, g->stream) != hipSuccess)
+                rc = GEM_EHIP;
+        }
+        if (rc) break;
+        std::vector<float> host(static_cast<size_t>(count * rows));
+        if (hipMemcpyAsync(host.data(), d_out, host.size() * sizeof(float), hipMemcpyDeviceToHost,
+                           g->stream) != hipSuccess ||
+            hipStreamSynchronize(g->stream) != hipSuccess) { rc = GEM_EHIP; break; }
+        if (theta_out) std::memcpy(theta_out, host.data(), static_cast<size_t>(count) * sizeof(float));
+        if (S_out) std::memcpy(S_out, host.data() + count, static_cast<size_t>(count * g->n) * sizeof(float));
+        if (M_out)
+            std::memcpy(M_out, host.data() + count * (1 + g->n),
+                        static_cast<size_t>(count * g->n) * sizeof(float));
+    } while (false);
+    (void)hipStreamSynchronize(g->stream);
+    (void)hipFree(d_idx);
+    (void)hipFree(d_out);
+    return rc;
+}
+
+int gem_clock(gem_t* g, int64_t* t)
+{
+    if (!g || !t) return GEM_EINVAL;
+    *t = g->t;
+    return GEM_OK;
+}
+
+int gem_pull_clocks(gem_t* g, int64_t* out)
+{
+    if (!g || !out) return GEM_EINVAL;
+    std::memcpy(out, g->pc.data(), g->pc.size() * sizeof(int64_t));
+    return GEM_OK;
+}
+
+int gem_reset_worker(gem_t* g, int32_t w)
+{
+    if (!g) return GEM_EINVAL;
+    if (w < 0 || w >= g->n) return GEM_EWORKER;
+    const size_t row = static_cast<size_t>(g->Pp) * sizeof(float);
+    GEM_HIP(hipMemcpyAsync(g->S + static_cast<int64_t>(w) * g->Pp, g->theta, row,
+                           hipMemcpyDeviceToDevice, g->stream));
+    GEM_HIP(hipMemsetAsync(g->M + static_cast<int64_t>(w) * g->Pp, 0, row, g->stream));
+    g->pc[w] = g->t;
+    return GEM_OK;
+}
+
+int gem_diag_enable(gem_t* g, int32_t on)
+{
+    if (!g) return GEM_EINVAL;
+    g->diag_on = on != 0;
+    return GEM_OK;
+}
+
+int gem_diag_reset(gem_t* g)
+{
+    if (!g) return GEM_EINVAL;
+    GEM_HIP(hipMemsetAsync(g->acc, 0, 8 * sizeof(double), g->stream));
+    g->diag_commits = 0;
+    return GEM_OK;
+}
+
+int gem_diag(gem_t* g, gem_diag_t* out)
+{
+    if (!g || !out) return GEM_EINVAL;
+    GEM_HIP(hipMemsetAsync(g->acc + 4, 0, sizeof(double), g->stream));
+    if (g->have_problem) GEM_HIP(gemk::launch_loss(g->theta, g->h, g->ts, g->P, g->acc + 4, g->stream));
+    double host[5];
+    GEM_HIP(hipMemcpyAsync(host, g->acc, sizeof(host), hipMemcpyDeviceToHost, g->stream));
+    GEM_HIP(hipStreamSynchronize(g->stream));
+    out->sum_ek = host[0];
+    out->sum_proxy = host[1];
+    out->n_clamped = static_cast<int64_t>(host[2]);
+    out->n_elem_commits = static_cast<int64_t>(host[3]);
+    out->loss = host[4];
+    out->n_commits = g->diag_commits;
+    return GEM_OK;
+}
+
+int gem_stats(gem_t* g, gem_stats_t* out)
+{
+    if (!g || !out) return GEM_EINVAL;
+    *out = g->stats;
+    return GEM_OK;
+}
+
+int gem_stats_reset(gem_t* g)
+{
+    if (!g) return GEM_EINVAL;
+    g->stats = gem_stats_t{};
+    return GEM_OK;
+}
+
+int gem_sync(gem_t* g)
+{
+    if (!g) return GEM_EINVAL;
+    GEM_HIP(hipStreamSynchronize(g->stream));
+    return GEM_OK;
+}
+
+int gem_copy_f32(const float* src, float* dst, int64_t count, void* stream)
+{
+    if (!src || !dst || count < 0) return GEM_EINVAL;
+    if (!aligned(src, 16) || !aligned(dst, 16)) return GEM_EALIGN;
+    GEM_HIP(gemk::launch_copy(src, dst, count, static_cast<hipStream_t>(stream)));
+    return GEM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Queuing schedule (host).  Philox4x32-10 draws keyed by the seed with
+// counter (w, k lo, k hi, tag); tag 1 = job times, tag 2 = per-worker means.
+// ---------------------------------------------------------------------------
+namespace {
+
+void sched_words(uint64_t seed, uint32_t w, uint64_t k, uint32_t tag, uint32_t x[4])
+{
+    const gemk::Words4 r = gemk::philox10(w, static_cast<uint32_t>(k), static_cast<uint32_t>(k >> 32),
+                                          tag, static_cast<uint32_t>(seed),
+                                          static_cast<uint32_t>(seed >> 32));
+    x[0] = r.x0; x[1] = r.x1; x[2] = r.x2; x[3] = r.x3;
+}
+
+uint64_t bits53(uint32_t a, uint32_t b)
+{
+    return (static_cast<uint64_t>(a >> 11) << 32) | static_cast<uint64_t>(b);
+}
+
+double unit_open0(uint32_t a, uint32_t b) { return static_cast<double>(bits53(a, b) + 1u) * 0x1p-53; }
+double unit_closed0(uint32_t a, uint32_t b) { return static_cast<double>(bits53(a, b)) * 0x1p-53; }
+
+double mean_of_worker(const gem_schedule_law& L, uint64_t seed, int32_t w)
+{
+    uint32_t x[4];
+    sched_words(seed, static_cast<uint32_t>(w), 0, 2u, x);
+    switch (L.law) {
+    case GEM_LAW_EXP_UNIFORM_MEAN:
+        return L.p0 + (L.p1 - L.p0) * unit_closed0(x[0], x[1]);
+    case GEM_LAW_EXP_LOGNORMAL_MEAN: {
+        const double u = unit_open0(x[0], x[1]);
+        const double v = unit_closed0(x[2], x[3]);
+        const double z = std::sqrt(-2.0 * std::log(u)) * std::cos(6.283185307179586 * v);
+        return std::exp(L.p0 + L.p1 * z);
+    }
+    default:
+        return 1.0;
+    }
+}
+
+double job_duration(const gem_schedule_law& L, double mean_w, uint64_t seed, int32_t w, int64_t k)
+{
+    uint32_t x[4];
+    sched_words(seed, static_cast<uint32_t>(w), static_cast<uint64_t>(k), 1u, x);
+    const double u = unit_open0(x[0], x[1]);
+    if (L.law == GEM_LAW_PARETO) return L.p1 * std::pow(u, -1.0 / L.p0);
+    return -mean_w * std::log(u);
+}
+
+}  // namespace
+
+int gem_schedule_make(int32_t n, int64_t T, const gem_schedule_law* law, uint64_t seed,
+                      int32_t pull_mode, int32_t* worker, int32_t* tau)
+{
+    if (n < 1 || T < 0 || !law || (T > 0 && (!worker || !tau))) return GEM_EINVAL;
+    if (pull_mode != GEM_PULL_POST_COMMIT && pull_mode != GEM_PULL_PRE_COMMIT) return GEM_EINVAL;
+    if (law->law < GEM_LAW_EXP || law->law > GEM_LAW_PARETO) return GEM_EINVAL;
+    if (law->law == GEM_LAW_PARETO && !(law->p0 > 0.0 && law->p1 > 0.0)) return GEM_EINVAL;
+    std::vector<double> mean(static_cast<size_t>(n)), finish(static_cast<size_t>(n));
+    std::vector<int64_t> jobs(static_cast<size_t>(n), 1), pulled(static_cast<size_t>(n), 0);
+    for (int32_t w = 0; w < n; ++w) {
+        mean[w] = mean_of_worker(*law, seed, w);
+        finish[w] = job_duration(*law, mean[w], seed, w, 0);
+    }
+    for (int64_t t = 0; t < T; ++t) {
+        int32_t best = 0;
+        for (int32_t w = 1; w < n; ++w)
+            if (finish[w] < finish[best]) best = w;
+        worker[t] = best;
+        const int64_t st = t - pulled[best];
+        if (st > INT32_MAX) return GEM_EINVAL;
+        tau[t] = static_cast<int32_t>(st);
+        pulled[best] = pull_mode == GEM_PULL_PRE_COMMIT ? t : t + 1;
+        finish[best] = finish[best] + job_duration(*law, mean[best], seed, best, jobs[best]);
+        jobs[best] += 1;
+    }
+    return GEM_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Checkpoints: a small header, then theta, S rows, M rows (P floats each),
+// the pull clocks and, if set, h and theta*.
+// ---------------------------------------------------------------------------
+namespace {
+
+struct CkptHeader {
+    char magic[8];
+    int64_t P;
+    int32_t n;
+    int32_t have_problem;
+    int64_t t;
+    gem_hyperparams hp;
+    gem_sim_params sp;
+};
+
+int write_rows(gem_handle* g, FILE* f, const float* dev, int64_t rows, std::vector<float>& buf)
+{
+    for (int64_t r = 0; r < rows; ++r) {
+        GEM_HIP(hipMemcpyAsync(buf.data(), dev + r * g->Pp, static_cast<size_t>(g->P) * sizeof(float),
+                               hipMemcpyDeviceToHost, g->stream));
+        GEM_HIP(hipStreamSynchronize(g->stream));
+        if (std::fwrite(buf.data(), sizeof(float), static_cast<size_t>(g->P), f) !=
+            static_cast<size_t>(g->P))
+            return GEM_EIO;
+    }
+    return GEM_OK;
+}
+
+int read_rows(gem_handle* g, FILE* f, float* dev, int64_t rows, std::vector<float>& buf)
+{
+    for (int64_t r = 0; r < rows; ++r) {
+        if (std::fread(buf.data(), sizeof(float), static_cast<size_t>(g->P), f) !=
+            static_cast<size_t>(g->P))
+            return GEM_EIO;
+        GEM_HIP(hipMemcpyAsync(dev + r * g->Pp, buf.data(), static_cast<size_t>(g->P) * sizeof(float),
+                               hipMemcpyHostToDevice, g->stream));
+        GEM_HIP(hipStreamSynchronize(g->stream));
+    }
+    return GEM_OK;
+}
+
+}  // namespace
+
+int gem_save(gem_t* g, const char* path)
+{
+    if (!g || !path) return GEM_EINVAL;
+    GEM_HIP(hipStreamSynchronize(g->stream));
+    FILE* f = std::fopen(path, "wb");
+    if (!f) return GEM_EIO;
+    CkptHeader hd;
+    std::memset(&hd, 0, sizeof(hd));
+    std::memcpy(hd.magic, "GEMCKPT1", 8);
+    hd.P = g->P;
+    hd.n = g->n;
+    hd.have_problem = g->have_problem ? 1 : 0;
+    hd.t = g->t;
+    hd.hp = g->hp;
+    hd.sp = g->sp;
+    std::vector<float> buf(static_cast<size_t>(g->P));
+    int rc = std::fwrite(&hd, sizeof(hd), 1, f) == 1 ? GEM_OK : GEM_EIO;
+    if (!rc) rc = write_rows(g, f, g->theta, 1, buf);
+    if (!rc) rc = write_rows(g, f, g->S, g->n, buf);
+    if (!rc) rc = write_rows(g, f, g->M, g->n, buf);
+    if (!rc && std::fwrite(g->pc.data(), sizeof(int64_t), g->pc.size(), f) != g->pc.size()) rc = GEM_EIO;
+    if (!rc && g->have_problem) rc = write_rows(g, f, g->h, 1, buf);
+    if (!rc && g->have_problem) rc = write_rows(g, f, g->ts, 1, buf);
+    if (std::fclose(f) != 0 && !rc) rc = GEM_EIO;
+    return rc;
+}
+
+int gem_load(gem_t* g, const char* path)
+{
+    if (!g || !path) return GEM_EINVAL;
+    FILE* f = std::fopen(path, "rb");
+    if (!f) return GEM_EIO;
+    CkptHeader hd;
+    int rc = std::fread(&hd, sizeof(hd), 1, f) == 1 ? GEM_OK : GEM_EIO;
+    if (!rc && (std::memcmp(hd.magic, "GEMCKPT1", 8) != 0 || hd.P != g->P || hd.n != g->n))
+        rc = GEM_EIO;
+    if (!rc && !valid_hp(hd.hp)) rc = GEM_EIO;
+    if (!rc) {
+        // The whole file must be there before any state is overwritten.
+        const int64_t rows = 1 + 2 * static_cast<int64_t>(g->n) + (hd.have_problem ? 2 : 0);
+        const int64_t want = static_cast<int64_t>(sizeof(hd)) + rows * g->P * 4 + 8 * static_cast<int64_t>(g->n);
+        if (std::fseek(f, 0, SEEK_END) != 0 || std::ftell(f) != want ||
+            std::fseek(f, static_cast<long>(sizeof(hd)), SEEK_SET) != 0)
+            rc = GEM_EIO;
+    }
+    if (!rc && hd.have_problem && !g->h) {
+        if (hipMalloc(&g->h, static_cast<size_t>(g->Pp) * sizeof(float)) != hipSuccess ||
+            hipMalloc(&g->ts, static_cast<size_t>(g->Pp) * sizeof(float)) != hipSuccess) {
+            (void)hipGetLastError();
+            rc = GEM_ENOMEM;
+        } else {
+            (void)hipMemsetAsync(g->h, 0, static_cast<size_t>(g->Pp) * sizeof(float), g->stream);
+            (void)hipMemsetAsync(g->ts, 0, static_cast<size_t>(g->Pp) * sizeof(float), g->stream);
+        }
+    }
+    std::vector<float> buf(static_cast<size_t>(g->P));
+    std::vector<int64_t> pc(static_cast<size_t>(g->n));
+    if (!rc) rc = read_rows(g, f, g->theta, 1, buf);
+    if (!rc) rc = read_rows(g, f, g->S, g->n, buf);
+    if (!rc) rc = read_rows(g, f, g->M, g->n, buf);
+    if (!rc && std::fread(pc.data(), sizeof(int64_t), pc.size(), f) != pc.size()) rc = GEM_EIO;
+    if (!rc && hd.have_problem) rc = read_rows(g, f, g->h, 1, buf);
+    if (!rc && hd.have_problem) rc = read_rows(g, f, g->ts, 1, buf);
+    std::fclose(f);
+    if (rc) return rc;
+    g->hp = hd.hp;
+    g->sp = hd.sp;
+    g->have_problem = hd.have_problem != 0;
+    g->t = hd.t;
+    g->pc = pc;
+    return GEM_OK;
+}
+
+}  // extern "C"

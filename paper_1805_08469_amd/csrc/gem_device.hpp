@@ -1,0 +1,145 @@
+// gem_device.hpp -- device-side numerics of the GEM commit pipeline (gfx950).
+//
+// Counter-based noise and the elementwise GEM step, evaluated in IEEE binary32
+// with round-to-nearest-even in a fixed operation order: explicit fma where
+// written, correctly rounded division and square root (hipcc's default on
+// gfx950), denormals kept, no contraction (built with -ffp-contract=off).
+// Any IEEE implementation of the same steps -- in particular the host-side
+// test oracle, written separately -- produces the same bits.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gemk {
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror & Shaw, SC'11).  Each round multiplies
+// words 0 and 2 by the two Philox multipliers and mixes the high halves with
+// the odd words and the key; the key advances by the two Weyl increments
+// after every round.
+// ---------------------------------------------------------------------------
+struct Words4 {
+    uint32_t x0, x1, x2, x3;
+};
+
+__host__ __device__ __forceinline__ Words4 philox10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                          uint32_t k0, uint32_t k1)
+{
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t pa = static_cast<uint64_t>(0xD2511F53u) * c0;
+        const uint64_t pb = static_cast<uint64_t>(0xCD9E8D57u) * c2;
+        const uint32_t y0 = static_cast<uint32_t>(pb >> 32) ^ c1 ^ k0;
+        const uint32_t y2 = static_cast<uint32_t>(pa >> 32) ^ c3 ^ k1;
+        c1 = static_cast<uint32_t>(pb);
+        c3 = static_cast<uint32_t>(pa);
+        c0 = y0;
+        c2 = y2;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return Words4{c0, c1, c2, c3};
+}
+
+// ---------------------------------------------------------------------------
+// Natural logarithm of u = k * 2^-24 for an integer k in [1, 2^24] (the Box-
+// Muller radius argument).  u = 2^e f with f in (sqrt(1/2), sqrt(2)];
+// ln f = 2 atanh((f-1)/(f+1)) by its series to the s^9 term (Abramowitz &
+// Stegun 4.1.27); ln u = e ln2 + ln f with ln 2 split into a 15-bit head and
+// a binary32 tail so that e * head is exact.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float ln_of_unit(float u)
+{
+    const uint32_t bits = __float_as_uint(u);
+    int e = static_cast<int>(bits >> 23) - 127;   // u > 0, so the sign bit is clear
+    const uint32_t mant = bits & 0x007FFFFFu;
+    const bool upper = mant > 0x003504F3u;        // 1.mant above sqrt(2) in binary32
+    const uint32_t fbits = mant | (upper ? 0x3F000000u : 0x3F800000u);
+    e += upper ? 1 : 0;
+    const float f = __uint_as_float(fbits);
+    const float s = (f - 1.0f) / (f + 1.0f);
+    const float z = s * s;
+    float p = 1.0f / 9.0f;
+    p = __builtin_fmaf(p, z, 1.0f / 7.0f);
+    p = __builtin_fmaf(p, z, 1.0f / 5.0f);
+    p = __builtin_fmaf(p, z, 1.0f / 3.0f);
+    p = p * z;
+    const float two_s = s + s;
+    const float ln_f = __builtin_fmaf(two_s, p, two_s);
+    const float ef = static_cast<float>(e);
+    const float ln2_tail = 0x1.7f7d1cp-20f;   // RN(ln 2 - ln2_head)
+    const float ln2_head = 0x1.62e4p-1f;
+    float r = __builtin_fmaf(ef, ln2_tail, ln_f);
+    r = __builtin_fmaf(ef, ln2_head, r);
+    return r;
+}
+
+// sin and cos of 2 pi k / 2^24, k in [0, 2^24).  The angle is reduced to the
+// nearest quarter turn on the integer, exactly; the rest, |x| <= pi/4, goes
+// through the Taylor series of sin (to x^9) and cos (to x^10).
+__device__ __forceinline__ void sincos_of_turn(uint32_t k, float& sn, float& cs)
+{
+    const uint32_t quarter = (k + 0x00200000u) >> 22;
+    const int rem = static_cast<int>(k) - static_cast<int>(quarter << 22);
+    const float step = 6.28318530717958647692f * 0x1p-24f;   // RN(2 pi) 2^-24
+    const float x = static_cast<float>(rem) * step;
+    const float x2 = x * x;
+
+    float ps = 1.0f / 362880.0f;
+    ps = __builtin_fmaf(ps, x2, -1.0f / 5040.0f);
+    ps = __builtin_fmaf(ps, x2, 1.0f / 120.0f);
+    ps = __builtin_fmaf(ps, x2, -1.0f / 6.0f);
+    ps = ps * x2;
+    const float sx = __builtin_fmaf(x, ps, x);
+
+    float pc = -1.0f / 3628800.0f;
+    pc = __builtin_fmaf(pc, x2, 1.0f / 40320.0f);
+    pc = __builtin_fmaf(pc, x2, -1.0f / 720.0f);
+    pc = __builtin_fmaf(pc, x2, 1.0f / 24.0f);
+    pc = __builtin_fmaf(pc, x2, -0.5f);
+    const float cx = __builtin_fmaf(pc, x2, 1.0f);
+
+    const uint32_t q = quarter & 3u;
+    const float a = (q & 1u) ? cx : sx;     // |sin| candidate
+    const float b = (q & 1u) ? sx : cx;     // |cos| candidate
+    sn = (q >= 2u) ? -a : a;
+    cs = (q == 1u || q == 2u) ? -b : b;
+}
+
+// Box-Muller (1958): from two words, u1 = ((xa >> 8) + 1) 2^-24 in (0, 1] and
+// the angle index xb >> 8, the pair r cos(phi), r sin(phi), r = sqrt(-2 ln u1).
+__device__ __forceinline__ void box_muller(uint32_t xa, uint32_t xb, float& zc, float& zs)
+{
+    const float u1 = static_cast<float>((xa >> 8) + 1u) * 0x1p-24f;
+    const float r = __builtin_sqrtf(-2.0f * ln_of_unit(u1));
+    float sn, cs;
+    sincos_of_turn(xb >> 8, sn, cs);
+    zc = r * cs;
+    zs = r * sn;
+}
+
+// Four standard normals for elements 4q..4q+3 at clock t.
+__device__ __forceinline__ float4 normals4(uint64_t q, uint32_t t, uint32_t k0, uint32_t k1)
+{
+    const Words4 w = philox10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), t, 0u,
+                              k0, k1);
+    float4 z;
+    box_muller(w.x0, w.x1, z.x, z.y);
+    box_muller(w.x2, w.x3, z.z, z.w);
+    return z;
+}
+
+// binary32 -> bfloat16 -> binary32, nearest-even; NaN stays a (quiet) NaN.
+__device__ __forceinline__ float round_to_bf16(float x)
+{
+    uint32_t b = __float_as_uint(x);
+    if ((b & 0x7FFFFFFFu) > 0x7F800000u) {
+        b = (b | 0x00400000u) & 0xFFFF0000u;
+    } else {
+        b = (b + 0x7FFFu + ((b >> 16) & 1u)) & 0xFFFF0000u;
+    }
+    return __uint_as_float(b);
+}
+
+}  // namespace gemk

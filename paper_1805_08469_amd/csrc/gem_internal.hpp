@@ -1,0 +1,71 @@
+// gem_internal.hpp -- pieces shared by the libgem host code and its kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/gem.h"
+
+namespace gemk {
+
+// Per-commit source / destination of a worker's (snapshot, moment) pair inside
+// one fused pass.  A worker's first commit in the pass reads its rows from HBM;
+// a later commit of the same worker reads the pair its previous commit left in
+// a register slot.  A worker's last commit in the pass writes the rows back;
+// an earlier one leaves the pair in a slot.
+constexpr int kHeldSlots = 8;
+constexpr uint8_t kFromHbm = 0x0F;   // low nibble: source slot, or kFromHbm
+constexpr uint8_t kToHbm = 0x0F;     // high nibble: destination slot, or kToHbm
+
+inline uint8_t route(uint8_t src, uint8_t dst) { return static_cast<uint8_t>(src | (dst << 4)); }
+
+// Runtime mode bits for the general kernel variant.
+enum : uint32_t {
+    kModeLiteralPi = 1u << 0,
+    kModeKappaMul = 1u << 1,     // multiply |m| by k_eff (kappa != 1 or SQRT form)
+    kModePrePull = 1u << 2,
+    kModeDownpour = 1u << 3,
+    kModeAdaptive = 1u << 4,
+};
+
+// Kernel argument block of one fused pass: K <= GEM_K_MAX commits at clocks
+// t0 .. t0 + K - 1 over the padded parameter vector.
+struct PassArgs {
+    float* theta;            // [Pp]
+    float* S;                // [n][Pp]
+    float* M;                // [n][Pp]
+    const float* h;          // [Pp]   (generated updates only)
+    const float* ts;         // [Pp]   theta*
+    double* diag;            // [4] accumulators (diagnostic variant only)
+    int64_t Pp;              // padded row length, a multiple of 64
+    int64_t P;               // true length
+    uint32_t key0, key1;     // noise seed
+    uint32_t t0;             // clock of the pass's first commit
+    int32_t K;
+    float neg_lr, sigma, mu, eps, k_eff;
+    uint32_t mode;
+    int32_t pad_;
+    int32_t worker[GEM_K_MAX];
+    int32_t tau[GEM_K_MAX];  // staleness (adaptive-staleness rule only)
+    uint8_t routes[GEM_K_MAX];
+    const void* upd[GEM_K_MAX];  // caller updates (given-update variants)
+};
+
+enum class Source { Generated = 0, GivenF32 = 1, GivenBF16 = 2 };
+
+// Launchers (defined in gem_kernels.hip).  `fast` selects the specialisation
+// for the default rule (GEM, CLAMP0, kappa_eff = 1, post-commit pull).
+hipError_t launch_pass(const PassArgs& a, Source src, bool fast, bool bf16_out, bool diag,
+                       hipStream_t stream);
+hipError_t launch_generate(const float* S_w, const float* h, const float* ts, void* out,
+                           bool bf16, int64_t P, uint32_t t, uint32_t key0, uint32_t key1,
+                           float neg_lr, float sigma, hipStream_t stream);
+hipError_t launch_fill_rows(float* dst, const float* row, int64_t Pp, int32_t rows,
+                            hipStream_t stream);
+hipError_t launch_gather(const float* src, const int64_t* idx, int64_t count, float* out,
+                         hipStream_t stream);
+hipError_t launch_loss(const float* theta, const float* h, const float* ts, int64_t P,
+                       double* out, hipStream_t stream);
+hipError_t launch_copy(const float* src, float* dst, int64_t count, hipStream_t stream);
+
+}  // namespace gemk

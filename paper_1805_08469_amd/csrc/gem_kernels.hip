@@ -1,0 +1,423 @@
+// gem_kernels.hip -- HIP kernels of the GEM commit pipeline for gfx950.
+//
+// The hot kernel is one fused pass: every thread owns four consecutive
+// parameters (one 16-byte chunk of every row) and applies the pass's K
+// commits to them in clock order.  theta, h and theta* are read once per
+// pass and theta written once; a committing worker's snapshot and moment rows
+// are read at its first commit in the pass and written at its last, the pair
+// living in registers in between.  Rows are read and written as 128-bit
+// accesses, consecutive lanes on consecutive chunks, so every wavefront moves
+// 1 KiB contiguous per row.  There is no contraction: the work is streaming
+// elementwise arithmetic (Philox, Box-Muller, the GEM step), bounded by HBM
+// bandwidth and VALU issue, so no MFMA is involved.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gem_device.hpp"
+#include "gem_internal.hpp"
+
+namespace gemk {
+
+namespace {
+
+constexpr int kBlock = 256;
+
+struct DiagAcc {
+    double ek = 0.0, proxy = 0.0, clamped = 0.0, elems = 0.0;
+};
+
+// One element of one commit.  th and m are the element's central value and
+// the committing worker's moment (in/out); s is its snapshot; d the update.
+// snap receives the value the worker's snapshot takes after this commit.
+template <bool FAST, bool DIAG>
+__device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float d, float s,
+                                               float& th, float& m, float& snap, bool live,
+                                               DiagAcc& acc)
+{
+    const float mn = __builtin_fmaf(a.mu, m, d);        // Alg. 1: m <- mu m + dtheta
+    const float drift = th - s;                         // theta_t - s_t (eq. 16)
+    float th_new;
+    float pi_raw = 0.0f;
+    bool gem_rule = true;
+    if (FAST) {
+        const float num = __builtin_fabsf(mn) - __builtin_fabsf(drift);
+        const float den = __builtin_fabsf(d) + a.eps;
+        pi_raw = num / den;                             // eq. 18 / Alg. 1
+        const float pi = (pi_raw > 0.0f) ? pi_raw : 0.0f;
+        th_new = __builtin_fmaf(pi, d, th);             // eq. 3
+        snap = th_new;
+    } else {
+        if (a.mode & kModeDownpour) {
+            gem_rule = false;
+            th_new = th + d;                            // eq. 1
+        } else if (a.mode & kModeAdaptive) {
+            gem_rule = false;
+            th_new = th + d / static_cast<float>(tau + 1);
+        } else {
+            const float km = (a.mode & kModeKappaMul) ? a.k_eff * __builtin_fabsf(mn)
+                                                      : __builtin_fabsf(mn);
+            const float num = km - __builtin_fabsf(drift);
+            const float den = __builtin_fabsf(d) + a.eps;
+            pi_raw = num / den;
+            const float pi = (a.mode & kModeLiteralPi) ? pi_raw
+                                                       : ((pi_raw > 0.0f) ? pi_raw : 0.0f);
+            th_new = __builtin_fmaf(pi, d, th);
+        }
+        snap = (a.mode & kModePrePull) ? th : th_new;
+    }
+    if (DIAG && live) {
+        const double e = static_cast<double>(th_new) - static_cast<double>(s);
+        const double kmd = static_cast<double>(FAST ? 1.0f : a.k_eff) * static_cast<double>(mn);
+        acc.ek += 0.5 * e * e;
+        acc.proxy += 0.5 * kmd * kmd;
+        if (gem_rule && !(pi_raw >= 0.0f)) acc.clamped += 1.0;
+        acc.elems += 1.0;
+    }
+    th = th_new;
+    m = mn;
+}
+
+// The simulated worker's update at snapshot s (notation table: -eta grad L(s)).
+template <bool BF16>
+__device__ __forceinline__ float stale_update(float neg_lr, float sigma, float s, float h, float ts,
+                                              float z)
+{
+    const float nz = sigma * z;
+    const float g = __builtin_fmaf(h, s - ts, nz);
+    float d = neg_lr * g;
+    if (BF16) d = round_to_bf16(d);
+    return d;
+}
+
+__device__ __forceinline__ float bf16_bits_to_float(uint32_t b16) { return __uint_as_float(b16 << 16); }
+
+// A caller update for chunk c: four elements, masked past the true length.
+template <Source SRC>
+__device__ __forceinline__ float4 load_given(const void* base, int64_t c, int64_t P)
+{
+    const int64_t i0 = c * 4;
+    if (SRC == Source::GivenF32) {
+        const float* p = static_cast<const float*>(base);
+        if (i0 + 4 <= P) return *reinterpret_cast<const float4*>(p + i0);
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (i0 + 0 < P) v.x = p[i0 + 0];
+        if (i0 + 1 < P) v.y = p[i0 + 1];
+        if (i0 + 2 < P) v.z = p[i0 + 2];
+        if (i0 + 3 < P) v.w = p[i0 + 3];
+        return v;
+    } else {
+        const uint16_t* p = static_cast<const uint16_t*>(base);
+        if (i0 + 4 <= P) {
+            const uint2 u = *reinterpret_cast<const uint2*>(p + i0);
+            return make_float4(bf16_bits_to_float(u.x & 0xFFFFu), bf16_bits_to_float(u.x >> 16),
+                               bf16_bits_to_float(u.y & 0xFFFFu), bf16_bits_to_float(u.y >> 16));
+        }
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (i0 + 0 < P) v.x = bf16_bits_to_float(p[i0 + 0]);
+        if (i0 + 1 < P) v.y = bf16_bits_to_float(p[i0 + 1]);
+        if (i0 + 2 < P) v.z = bf16_bits_to_float(p[i0 + 2]);
+        if (i0 + 3 < P) v.w = bf16_bits_to_float(p[i0 + 3]);
+        return v;
+    }
+}
+
+struct Pair {
+    float4 s, m;
+};
+
+template <Source SRC, bool FAST, bool BF16, bool DIAG>
+__global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
+{
+    const int64_t nchunk = a.Pp >> 2;
+    const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const bool active = c < nchunk;
+    if (!DIAG && !active) return;
+    const int64_t cc = active ? c : 0;   // inactive lanes (diagnostic variant) do no memory work
+
+    const int64_t off = cc * 4;
+    float4 th = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 hh = th, tt = th;
+    if (active) {
+        th = *reinterpret_cast<const float4*>(a.theta + off);
+        if (SRC == Source::Generated) {
+            hh = *reinterpret_cast<const float4*>(a.h + off);
+            tt = *reinterpret_cast<const float4*>(a.ts + off);
+        }
+    }
+
+    Pair held0, held1, held2, held3, held4, held5, held6, held7;
+    Pair next;
+    const int K = a.K;
+    if (active && (a.routes[0] & 0x0F) == kFromHbm) {
+        const int64_t row = static_cast<int64_t>(a.worker[0]) * a.Pp + off;
+        next.s = *reinterpret_cast<const float4*>(a.S + row);
+        next.m = *reinterpret_cast<const float4*>(a.M + row);
+    }
+
+    DiagAcc acc;
+    const bool l0 = off + 0 < a.P, l1 = off + 1 < a.P, l2 = off + 2 < a.P, l3 = off + 3 < a.P;
+
+    for (int j = 0; j < K; ++j) {
+        const uint32_t r = a.routes[j];
+        const uint32_t src = r & 0x0Fu;
+        const uint32_t dst = r >> 4;
+        const int w = a.worker[j];
+        Pair cur;
+        if (src == kFromHbm) {
+            cur = next;
+        } else {
+            switch (src) {
+            case 0: cur = held0; break;
+            case 1: cur = held1; break;
+            case 2: cur = held2; break;
+            case 3: cur = held3; break;
+            case 4: cur = held4; break;
+            case 5: cur = held5; break;
+            case 6: cur = held6; break;
+            default: cur = held7; break;
+            }
+        }
+        // Prefetch the next commit's rows if they come from HBM.  Such a row
+        // belongs to a worker not yet seen in this pass, so no store of this
+        // pass precedes it.
+        if (active && j + 1 < K && (a.routes[j + 1] & 0x0F) == kFromHbm) {
+            const int64_t row = static_cast<int64_t>(a.worker[j + 1]) * a.Pp + off;
+            next.s = *reinterpret_cast<const float4*>(a.S + row);
+            next.m = *reinterpret_cast<const float4*>(a.M + row);
+        }
+
+        float4 d;
+        if (SRC == Source::Generated) {
+            const float4 z = normals4(static_cast<uint64_t>(cc), a.t0 + static_cast<uint32_t>(j),
+                                      a.key0, a.key1);
+            d.x = stale_update<BF16>(a.neg_lr, a.sigma, cur.s.x, hh.x, tt.x, z.x);
+            d.y = stale_update<BF16>(a.neg_lr, a.sigma, cur.s.y, hh.y, tt.y, z.y);
+            d.z = stale_update<BF16>(a.neg_lr, a.sigma, cur.s.z, hh.z, tt.z, z.z);
+            d.w = stale_update<BF16>(a.neg_lr, a.sigma, cur.s.w, hh.w, tt.w, z.w);
+        } else {
+            d = active ? load_given<SRC>(a.upd[j], cc, a.P) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+
+        const int tau = a.tau[j];
+        Pair out;
+        out.m = cur.m;
+        commit_element<FAST, DIAG>(a, tau, d.x, cur.s.x, th.x, out.m.x, out.s.x, active && l0, acc);
+        commit_element<FAST, DIAG>(a, tau, d.y, cur.s.y, th.y, out.m.y, out.s.y, active && l1, acc);
+        commit_element<FAST, DIAG>(a, tau, d.z, cur.s.z, th.z, out.m.z, out.s.z, active && l2, acc);
+        commit_element<FAST, DIAG>(a, tau, d.w, cur.s.w, th.w, out.m.w, out.s.w, active && l3, acc);
+
+        if (dst == kToHbm) {
+            if (active) {
+                const int64_t row = static_cast<int64_t>(w) * a.Pp + off;
+                *reinterpret_cast<float4*>(a.S + row) = out.s;
+                *reinterpret_cast<float4*>(a.M + row) = out.m;
+            }
+        } else {
+            switch (dst) {
+            case 0: held0 = out; break;
+            case 1: held1 = out; break;
+            case 2: held2 = out; break;
+            case 3: held3 = out; break;
+            case 4: held4 = out; break;
+            case 5: held5 = out; break;
+            case 6: held6 = out; break;
+            default: held7 = out; break;
+            }
+        }
+    }
+    if (active) *reinterpret_cast<float4*>(a.theta + off) = th;
+
+    if (DIAG) {
+        __shared__ double red[4][kBlock];
+        red[0][threadIdx.x] = acc.ek;
+        red[1][threadIdx.x] = acc.proxy;
+        red[2][threadIdx.x] = acc.clamped;
+        red[3][threadIdx.x] = acc.elems;
+        __syncthreads();
+        for (int step = kBlock / 2; step > 0; step >>= 1) {
+            if (static_cast<int>(threadIdx.x) < step) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) red[q][threadIdx.x] += red[q][threadIdx.x + step];
+            }
+            __syncthreads();
+        }
+        if (threadIdx.x < 4) atomicAdd(&a.diag[threadIdx.x], red[threadIdx.x][0]);
+    }
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kBlock) void generate_kernel(const float* __restrict__ S_w,
+                                                         const float* __restrict__ h,
+                                                         const float* __restrict__ ts, void* out,
+                                                         int64_t P, uint32_t t, uint32_t key0,
+                                                         uint32_t key1, float neg_lr, float sigma)
+{
+    const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const int64_t i0 = c * 4;
+    if (i0 >= P) return;
+    const float4 s = *reinterpret_cast<const float4*>(S_w + i0);
+    const float4 hv = *reinterpret_cast<const float4*>(h + i0);
+    const float4 tv = *reinterpret_cast<const float4*>(ts + i0);
+    const float4 z = normals4(static_cast<uint64_t>(c), t, key0, key1);
+    float d[4];
+    d[0] = stale_update<BF16>(neg_lr, sigma, s.x, hv.x, tv.x, z.x);
+    d[1] = stale_update<BF16>(neg_lr, sigma, s.y, hv.y, tv.y, z.y);
+    d[2] = stale_update<BF16>(neg_lr, sigma, s.z, hv.z, tv.z, z.z);
+    d[3] = stale_update<BF16>(neg_lr, sigma, s.w, hv.w, tv.w, z.w);
+    if (BF16) {
+        uint16_t* o = static_cast<uint16_t*>(out);
+        if (i0 + 4 <= P) {
+            uint2 u;
+            u.x = (__float_as_uint(d[0]) >> 16) | (__float_as_uint(d[1]) & 0xFFFF0000u);
+            u.y = (__float_as_uint(d[2]) >> 16) | (__float_as_uint(d[3]) & 0xFFFF0000u);
+            *reinterpret_cast<uint2*>(o + i0) = u;
+        } else {
+            for (int k = 0; k < 4; ++k)
+                if (i0 + k < P) o[i0 + k] = static_cast<uint16_t>(__float_as_uint(d[k]) >> 16);
+        }
+    } else {
+        float* o = static_cast<float*>(out);
+        if (i0 + 4 <= P) {
+            *reinterpret_cast<float4*>(o + i0) = make_float4(d[0], d[1], d[2], d[3]);
+        } else {
+            for (int k = 0; k < 4; ++k)
+                if (i0 + k < P) o[i0 + k] = d[k];
+        }
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void fill_rows_kernel(float* dst, const float* row, int64_t Pp,
+                                                           int32_t rows)
+{
+    const int64_t nchunk = Pp >> 2;
+    const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (c >= nchunk) return;
+    const float4 v = reinterpret_cast<const float4*>(row)[c];
+    for (int32_t r = 0; r < rows; ++r) reinterpret_cast<float4*>(dst + static_cast<int64_t>(r) * Pp)[c] = v;
+}
+
+__global__ __launch_bounds__(kBlock) void gather_kernel(const float* __restrict__ src,
+                                                        const int64_t* __restrict__ idx,
+                                                        int64_t count, float* __restrict__ out)
+{
+    const int64_t k = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (k < count) out[k] = src[idx[k]];
+}
+
+__global__ __launch_bounds__(kBlock) void loss_kernel(const float* __restrict__ theta,
+                                                      const float* __restrict__ h,
+                                                      const float* __restrict__ ts, int64_t P,
+                                                      double* out)
+{
+    __shared__ double red[kBlock];
+    double acc = 0.0;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < P;
+         i += static_cast<int64_t>(gridDim.x) * kBlock) {
+        const double e = static_cast<double>(theta[i]) - static_cast<double>(ts[i]);
+        acc += 0.5 * static_cast<double>(h[i]) * e * e;
+    }
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    for (int step = kBlock / 2; step > 0; step >>= 1) {
+        if (static_cast<int>(threadIdx.x) < step) red[threadIdx.x] += red[threadIdx.x + step];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) atomicAdd(out, red[0]);
+}
+
+__global__ __launch_bounds__(kBlock) void copy_kernel(const float* __restrict__ src,
+                                                      float* __restrict__ dst, int64_t count)
+{
+    const int64_t n4 = count / 4;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    const int64_t first = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    for (int64_t k = first; k < n4; k += stride)
+        reinterpret_cast<float4*>(dst)[k] = reinterpret_cast<const float4*>(src)[k];
+    if (first < count - n4 * 4) dst[n4 * 4 + first] = src[n4 * 4 + first];
+}
+
+inline unsigned blocks_for(int64_t items) {
+    return static_cast<unsigned>((items + kBlock - 1) / kBlock);
+}
+
+template <Source SRC, bool FAST, bool BF16, bool DIAG>
+hipError_t launch_one(const PassArgs& a, hipStream_t st)
+{
+    hipLaunchKernelGGL((pass_kernel<SRC, FAST, BF16, DIAG>), dim3(blocks_for(a.Pp >> 2)),
+                       dim3(kBlock), 0, st, a);
+    return hipGetLastError();
+}
+
+template <Source SRC, bool BF16>
+hipError_t launch_fd(const PassArgs& a, bool fast, bool diag, hipStream_t st)
+{
+    if (fast) return diag ? launch_one<SRC, true, BF16, true>(a, st) : launch_one<SRC, true, BF16, false>(a, st);
+    return diag ? launch_one<SRC, false, BF16, true>(a, st) : launch_one<SRC, false, BF16, false>(a, st);
+}
+
+}  // namespace
+
+hipError_t launch_pass(const PassArgs& a, Source src, bool fast, bool bf16_out, bool diag,
+                       hipStream_t stream)
+{
+    switch (src) {
+    case Source::Generated:
+        return bf16_out ? launch_fd<Source::Generated, true>(a, fast, diag, stream)
+                        : launch_fd<Source::Generated, false>(a, fast, diag, stream);
+    case Source::GivenF32:
+        return launch_fd<Source::GivenF32, false>(a, fast, diag, stream);
+    case Source::GivenBF16:
+        return launch_fd<Source::GivenBF16, false>(a, fast, diag, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_generate(const float* S_w, const float* h, const float* ts, void* out, bool bf16,
+                           int64_t P, uint32_t t, uint32_t key0, uint32_t key1, float neg_lr,
+                           float sigma, hipStream_t stream)
+{
+    const unsigned grid = blocks_for((P + 3) / 4);
+    if (bf16)
+        hipLaunchKernelGGL(generate_kernel<true>, dim3(grid), dim3(kBlock), 0, stream, S_w, h, ts,
+                           out, P, t, key0, key1, neg_lr, sigma);
+    else
+        hipLaunchKernelGGL(generate_kernel<false>, dim3(grid), dim3(kBlock), 0, stream, S_w, h, ts,
+                           out, P, t, key0, key1, neg_lr, sigma);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_rows(float* dst, const float* row, int64_t Pp, int32_t rows, hipStream_t stream)
+{
+    hipLaunchKernelGGL(fill_rows_kernel, dim3(blocks_for(Pp >> 2)), dim3(kBlock), 0, stream, dst,
+                       row, Pp, rows);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather(const float* src, const int64_t* idx, int64_t count, float* out,
+                         hipStream_t stream)
+{
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(gather_kernel, dim3(blocks_for(count)), dim3(kBlock), 0, stream, src, idx,
+                       count, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_loss(const float* theta, const float* h, const float* ts, int64_t P, double* out,
+                       hipStream_t stream)
+{
+    const int64_t want = blocks_for(P);
+    const unsigned grid = static_cast<unsigned>(want < 4096 ? (want > 0 ? want : 1) : 4096);
+    hipLaunchKernelGGL(loss_kernel, dim3(grid), dim3(kBlock), 0, stream, theta, h, ts, P, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy(const float* src, float* dst, int64_t count, hipStream_t stream)
+{
+    if (count <= 0) return hipSuccess;
+    const int64_t want = blocks_for(count / 4 > 0 ? count / 4 : 1);
+    const unsigned grid = static_cast<unsigned>(want < 65536 ? want : 65536);
+    hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(kBlock), 0, stream, src, dst, count);
+    return hipGetLastError();
+}
+
+}  // namespace gemk

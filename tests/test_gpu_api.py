@@ -1,0 +1,158 @@
+"""GPU tests of the commit entry points that take caller updates
+(gem_commit, gem_commit_batch in fp32 and bf16), of the generator-then-commit
+pipeline, and of the error paths: a rejected call must leave the state and
+the clock untouched."""
+import numpy as np
+import pytest
+
+import oracle as O
+from gpu_util import assert_parity
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1805_08469_amd import gem
+    return torch, gem
+
+
+def _updates(rng, K, P, scale=1e-2):
+    return (rng.standard_normal((K, P)) * scale).astype(np.float32)
+
+
+def _device_rows(torch, a):
+    """Upload a [K, P] array with its row stride padded to 8 elements, so each
+    row starts 16-byte aligned (fp32) / 8-byte aligned (bf16) as gem.h requires."""
+    K, P = a.shape
+    stride = -(-P // 8) * 8
+    pad = np.zeros((K, stride), dtype=a.dtype)
+    pad[:, :P] = a
+    return torch.from_numpy(pad).cuda()
+
+
+def _to_bf16_bits(x):
+    b = O.round_bf16(x).view(np.uint32)
+    return (b >> 16).astype(np.uint16)
+
+
+@pytest.mark.parametrize("P", [7, 4096, 100_003])
+def test_commit_one_by_one(env, P):
+    torch, G = env
+    n, T = 4, 40
+    rng = np.random.default_rng(P)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=1)
+    d = _updates(rng, T, P)
+    dev = _device_rows(torch, d)
+    with G.Gem(P, n) as g:
+        for j in range(T):
+            g.commit(dev[j].data_ptr(), int(worker[j]))
+        theta, S, M = g.theta(), g.S(), g.M()
+    st = O.State.initial(n, P)
+    O.commit_given(O.Hyper(), st, worker, d, tau=tau)
+    assert_parity("theta", theta, st.theta)
+    assert_parity("S", S, st.S)
+    assert_parity("M", M, st.M)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("K", [1, 5, 32, 45])
+def test_commit_batch(env, dtype, K):
+    torch, G = env
+    P, n = 10_007, 3                      # n = 3: workers repeat inside every batch
+    rng = np.random.default_rng(K)
+    worker, tau = G.gem_schedule_make(n, 3 * K, G.GEM_LAW_EXP, seed=K)
+    d = _updates(rng, 3 * K, P)
+    if dtype == "bf16":
+        bits = _to_bf16_bits(d)
+        dev = _device_rows(torch, bits.view(np.int16))
+        code = G.GEM_BF16
+        ref_upd = bits
+    else:
+        dev = _device_rows(torch, d)
+        code = G.GEM_F32
+        ref_upd = d
+    with G.Gem(P, n) as g:
+        for b in range(3):
+            rows = range(b * K, (b + 1) * K)
+            g.commit_batch([dev[j].data_ptr() for j in rows], code, worker[b * K:(b + 1) * K],
+                           tau[b * K:(b + 1) * K])
+        theta, S, M, clock = g.theta(), g.S(), g.M(), g.clock
+    st = O.State.initial(n, P)
+    O.commit_given(O.Hyper(), st, worker, ref_upd, tau=tau)
+    assert clock == 3 * K
+    assert_parity("theta", theta, st.theta)
+    assert_parity("S", S, st.S)
+    assert_parity("M", M, st.M)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_generate_then_commit_equals_fused_run(env, bf16):
+    """The unfused pipeline (generator kernel writes dtheta, commit kernel reads
+    it) equals the fused simulated run."""
+    torch, G = env
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T = 6000, 5, 64
+    h, ts = make_problem(P, 1e-4, 1.0, 4)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=4)
+    code = G.GEM_BF16 if bf16 else G.GEM_F32
+    buf = torch.empty(P, dtype=torch.int16 if bf16 else torch.float32, device="cuda")
+    with G.Gem(P, n) as a, G.Gem(P, n) as b:
+        a.set_quadratic(h, ts, 0.01, 0.02, 8, bf16=bf16)
+        b.set_quadratic(h, ts, 0.01, 0.02, 8, bf16=bf16)
+        a.sim_run(worker, tau, 16)
+        for j in range(T):
+            assert G.gem_generate(b.h, int(worker[j]), buf.data_ptr(), code) == G.GEM_OK
+            b.commit_batch([buf.data_ptr()], code, worker[j:j + 1], tau[j:j + 1])
+        for x, y in ((a.theta(), b.theta()), (a.S(), b.S()), (a.M(), b.M())):
+            assert np.array_equal(x, y)
+
+
+def test_rejected_calls_change_nothing(env):
+    torch, G = env
+    P, n = 1000, 3
+    d = torch.ones(P + 8, dtype=torch.float32, device="cuda")
+    with G.Gem(P, n) as g:
+        g.commit(d.data_ptr(), 0)
+        before = (g.theta(), g.S(), g.M(), g.clock, g.pull_clocks())
+        assert G.gem_commit(g.h, d.data_ptr(), 3) == G.GEM_EWORKER
+        assert G.gem_commit(g.h, d.data_ptr(), -1) == G.GEM_EWORKER
+        assert G.gem_commit(g.h, d.data_ptr() + 4, 0) == G.GEM_EALIGN
+        assert G.gem_commit(g.h, 0, 0) == G.GEM_EINVAL
+        # worker 1's staleness at t=1 is 1; a batch with a wrong value in its
+        # second entry must not apply its first entry either
+        assert G.gem_commit_batch(g.h, [d.data_ptr()] * 2, G.GEM_F32, [1, 2], [1, 0]) == G.GEM_ESTALE
+        assert G.gem_commit_batch(g.h, [d.data_ptr()], 7, [1], None) == G.GEM_EDTYPE
+        assert G.gem_commit_batch(g.h, [d.data_ptr() + 2], G.GEM_BF16, [1], None) == G.GEM_EALIGN
+        assert G.gem_sim_run(g.h, [0], [0], 1) == G.GEM_ESTATE        # no problem set
+        assert G.gem_generate(g.h, 0, d.data_ptr(), G.GEM_F32) == G.GEM_ESTATE
+        g.set_quadratic(np.ones(P, np.float32), np.zeros(P, np.float32), 0.01, 0.0, 0)
+        assert G.gem_sim_run(g.h, [0], [0], 0) == G.GEM_EINVAL          # K = 0
+        assert G.gem_sim_run(g.h, [0], [0], 33) == G.GEM_EINVAL         # K > GEM_K_MAX
+        assert G.gem_sim_run(g.h, [0, 9], None, 4) == G.GEM_EWORKER
+        assert G.gem_reset_worker(g.h, 5) == G.GEM_EWORKER
+        after = (g.theta(), g.S(), g.M(), g.clock, g.pull_clocks())
+    for x, y in zip(before, after):
+        assert np.array_equal(x, y)
+
+
+def test_empty_batch_and_run_are_no_ops(env):
+    torch, G = env
+    with G.Gem(10, 2) as g:
+        g.set_quadratic(np.ones(10, np.float32), np.zeros(10, np.float32), 0.01, 0.1, 0)
+        assert G.gem_commit_batch(g.h, [], G.GEM_F32, np.zeros(0, np.int32), None) == G.GEM_OK
+        assert G.gem_sim_run(g.h, np.zeros(0, np.int32), None, 4) == G.GEM_OK
+        assert g.clock == 0 and np.all(g.theta() == 0)
+
+
+def test_copy_probe(env):
+    torch, G = env
+    for count in (1, 4, 1003, 1 << 20):
+        src = torch.randn(count, device="cuda")
+        dst = torch.zeros(count, device="cuda")
+        assert G.gem_copy_f32(src.data_ptr(), dst.data_ptr(), count) == G.GEM_OK
+        torch.cuda.synchronize()
+        assert torch.equal(src, dst)

@@ -1,0 +1,86 @@
+"""Parity at the workloads' full sizes, in the launch configuration the
+benchmark times (gem_sim_run over the whole schedule with the workload's K).
+
+The GPU runs every element; the oracle runs a sample of element indices (the
+first and last chunks, the ragged tail and random indices).  Each element's
+trajectory depends only on its own inputs, the schedule and the seed, so the
+oracle's subset run equals those entries of a full run (pinned on the CPU by
+test_subset_run_equals_full_run)."""
+import numpy as np
+import pytest
+
+import oracle as O
+from gpu_util import assert_parity
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def G():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1805_08469_amd import gem
+    return gem
+
+
+def _sample(P, k=2048, seed=0):
+    rng = np.random.default_rng(seed)
+    fixed = np.array([0, 1, 2, 3, 4, 5, 6, 7, P // 2, P - 8, P - 7, P - 6, P - 5, P - 4, P - 3,
+                      P - 2, P - 1])
+    idx = np.unique(np.concatenate([fixed[(fixed >= 0) & (fixed < P)],
+                                    rng.integers(0, P, size=k)]))
+    return idx.astype(np.int64)
+
+
+def _free_bytes():
+    import torch
+    free, _ = torch.cuda.mem_get_info()
+    return free
+
+
+def _workload_parity(G, name, T=None):
+    from paper_1805_08469_amd.workloads import WORKLOADS, problem
+    wl = WORKLOADS[name]
+    if T is not None:
+        wl = wl.with_(T=T)
+    need = 4 * wl.P * (2 * wl.n + 3) * 1.05
+    if _free_bytes() < need:
+        pytest.skip(f"{name} needs {need / 2**30:.1f} GiB of device memory")
+    h, ts = problem(wl)
+    worker, tau = G.gem_schedule_make(wl.n, wl.T, wl.law, wl.law_p0, wl.law_p1, seed=wl.seed)
+    idx = _sample(wl.P, seed=wl.P)
+    print(f"[{name}] P={wl.P} n={wl.n} T={wl.T} K={wl.K} bf16={wl.bf16} sample={idx.size}",
+          flush=True)
+    with G.Gem(wl.P, wl.n) as g:
+        g.set_quadratic(h, ts, wl.lr, wl.sigma, wl.seed, bf16=wl.bf16)
+        g.sim_run(worker, tau, wl.K)
+        theta, S, M = g.gather(idx)
+        pc = g.pull_clocks()
+        stats = g.stats()
+    hp = O.Hyper(lr=wl.lr, sigma=wl.sigma, momentum=wl.momentum, bf16=wl.bf16, seed=wl.seed)
+    st = O.State.initial(wl.n, idx.size)
+    O.run(hp, wl.P, st, idx, h[idx], ts[idx], worker, tau)
+    assert np.array_equal(pc, st.pc)
+    assert_parity(f"{name} theta", theta, st.theta)
+    assert_parity(f"{name} S", S, st.S)
+    assert_parity(f"{name} M", M, st.M)
+    return stats
+
+
+def test_small(G):
+    s = _workload_parity(G, "small")
+    assert s.passes == 10_000
+
+
+def test_resnet18(G):
+    _workload_parity(G, "resnet18")
+
+
+def test_headline(G):
+    s = _workload_parity(G, "headline")
+    assert s.passes == -(-5000 // 32)      # no pass is cut at this schedule
+
+
+def test_large(G):
+    _workload_parity(G, "large")

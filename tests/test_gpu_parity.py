@@ -1,0 +1,218 @@
+"""GPU parity of whole simulated runs (gem_sim_run) against the oracle:
+theta, every worker's snapshot S[w] and moment M[w], element by element, on
+the same seeded schedules and noise.  Covers the tiny workload end to end,
+fusion of K commits per pass (with workers repeating inside a pass and passes
+cut for register pressure), ragged parameter counts, every commit-rule mode,
+bfloat16 updates, diagnostics, checkpoint resume and worker restarts."""
+import os
+import tempfile
+
+import numpy as np
+import pytest
+
+import oracle as O
+from gpu_util import assert_parity, parity
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def G():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1805_08469_amd import gem
+    return gem
+
+
+def _hp(G, pi_mode=0, kappa=1.0, kappa_mode=0, pull=0, rule=0, momentum=0.9):
+    hp = G.gem_hyperparams_default()
+    hp.momentum, hp.kappa = momentum, kappa
+    hp.pi_mode, hp.kappa_mode, hp.pull_mode, hp.rule = pi_mode, kappa_mode, pull, rule
+    return hp
+
+
+def _ohp(hp, lr, sigma, seed, bf16=False):
+    return O.Hyper(lr=lr, sigma=sigma, momentum=hp.momentum, eps=1e-16, kappa=hp.kappa,
+                   pi_mode=hp.pi_mode, kappa_mode=hp.kappa_mode, pull_mode=hp.pull_mode,
+                   rule=hp.rule, bf16=bf16, seed=seed)
+
+
+def _run_both(G, P, n, worker, tau, K, hp, lr=0.01, sigma=0.1, seed=7, bf16=False,
+              h_lo=1e-3, pseed=1):
+    from paper_1805_08469_amd.workloads import make_problem
+    h, ts = make_problem(P, h_lo, 1.0, pseed)
+    with G.Gem(P, n, hp) as g:
+        g.set_quadratic(h, ts, lr, sigma, seed, bf16=bf16)
+        g.sim_run(worker, tau, K)
+        out = (g.theta(), g.S(), g.M(), g.pull_clocks(), g.clock, g.stats())
+    st = O.State.initial(n, P)
+    O.run(_ohp(hp, lr, sigma, seed, bf16), P, st, np.arange(P), h, ts, worker, tau)
+    return out, st
+
+
+def _check(out, st, tag=""):
+    theta, S, M, pc, clock, _ = out
+    assert clock == st.t
+    assert np.array_equal(pc, st.pc), f"{tag} pull clocks"
+    assert_parity(f"{tag} theta", theta, st.theta)
+    assert_parity(f"{tag} S", S, st.S)
+    assert_parity(f"{tag} M", M, st.M)
+
+
+def test_tiny_workload_full(G):
+    from paper_1805_08469_amd.workloads import WORKLOADS
+    wl = WORKLOADS["tiny"]
+    worker, tau = G.gem_schedule_make(wl.n, wl.T, wl.law, wl.law_p0, wl.law_p1, seed=wl.seed)
+    out, st = _run_both(G, wl.P, wl.n, worker, tau, wl.K, _hp(G), wl.lr, wl.sigma, wl.seed,
+                        h_lo=wl.h_lo, pseed=wl.seed)
+    _check(out, st, "tiny")
+    assert out[5].passes == wl.T       # K = 1: one pass per commit
+
+
+@pytest.mark.parametrize("K", [1, 2, 3, 8, 16, 32])
+def test_fusion_is_invisible(G, K):
+    """K commits per pass equal K single commits, bit for bit, including
+    workers that commit several times inside one pass."""
+    P, n, T = 3000, 3, 300
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=5)
+    out, st = _run_both(G, P, n, worker, tau, K, _hp(G))
+    _check(out, st, f"K={K}")
+    assert out[5].passes == -(-T // K)   # n = 3 never needs more than 3 held slots
+
+
+def test_register_pressure_cuts_passes(G):
+    """Twelve workers in round robin keep up to 11 pairs in flight inside a
+    32-commit pass; the planner cuts passes so that at most 8 are held, and
+    the result is still the sequential one."""
+    P, n, T = 2048, 12, 240
+    worker = np.tile(np.arange(n, dtype=np.int32), T // n)
+    tau = np.array([t if t < n else n - 1 for t in range(T)], dtype=np.int32)
+    out, st = _run_both(G, P, n, worker, tau, 32, _hp(G))
+    _check(out, st, "round robin")
+    assert out[5].passes > -(-T // 32)
+
+
+@pytest.mark.parametrize("P", [1, 3, 63, 64, 65, 1000, 4133, 70001])
+def test_ragged_sizes(G, P):
+    n, T = 5, 60
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=P)
+    out, st = _run_both(G, P, n, worker, tau, 8, _hp(G))
+    _check(out, st, f"P={P}")
+
+
+MODES = {
+    "literal": dict(pi_mode=1),
+    "kappa2_linear": dict(kappa=2.0),
+    "kappa3_sqrt": dict(kappa=3.0, kappa_mode=1),
+    "kappa_half": dict(kappa=0.5),
+    "pre_commit_pull": dict(pull=1),
+    "downpour": dict(rule=1),
+    "adaptive": dict(rule=2),
+    "mu0": dict(momentum=0.0),
+}
+
+
+@pytest.mark.parametrize("mode", sorted(MODES))
+@pytest.mark.parametrize("K", [1, 16])
+def test_modes(G, mode, K):
+    P, n, T = 4096 + 17, 6, 80
+    hp = _hp(G, **MODES[mode])
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=3, pull_mode=hp.pull_mode)
+    out, st = _run_both(G, P, n, worker, tau, K, hp)
+    _check(out, st, mode)
+
+
+@pytest.mark.parametrize("K", [1, 16])
+def test_bf16_updates(G, K):
+    P, n, T = 5000, 10, 120
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_PARETO, 1.5, 1 / 3, seed=11)
+    out, st = _run_both(G, P, n, worker, tau, K, _hp(G), sigma=0.02, bf16=True)
+    _check(out, st, "bf16")
+
+
+def test_literal_diverges_on_gpu_like_oracle(G):
+    """The LITERAL pi blows up on the tiny workload (reading R8); the GPU follows the
+    oracle into the blow-up as long as values stay finite."""
+    from paper_1805_08469_amd.workloads import WORKLOADS
+    wl = WORKLOADS["tiny"]
+    T = 150
+    worker, tau = G.gem_schedule_make(wl.n, T, wl.law, seed=wl.seed)
+    out, st = _run_both(G, wl.P, wl.n, worker, tau, 1, _hp(G, pi_mode=1), wl.lr, wl.sigma,
+                        wl.seed, h_lo=wl.h_lo, pseed=wl.seed)
+    _check(out, st, "literal")
+    assert np.nanmax(np.abs(st.theta)) > 1e6
+
+
+def test_diagnostics_match_oracle(G):
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T, K = 10_000 + 3, 8, 200, 8
+    h, ts = make_problem(P, 1e-3, 1.0, 2)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=2)
+    hp = _hp(G)
+    with G.Gem(P, n, hp) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 4)
+        G.gem_diag_enable(g.h, True)
+        g.sim_run(worker, tau, K)
+        d = G.gem_diag(g.h)
+    st = O.State.initial(n, P)
+    dg, _ = O.run(_ohp(hp, 0.01, 0.1, 4), P, st, np.arange(P), h, ts, worker, tau, diag=True)
+    assert d.n_commits == T
+    assert d.n_elem_commits == P * T
+    assert d.n_clamped == int(dg["n_clamped"].sum())
+    assert d.sum_ek == pytest.approx(float(dg["sum_ek"].sum()), rel=1e-9)
+    assert d.sum_proxy == pytest.approx(float(dg["sum_proxy"].sum()), rel=1e-9)
+    assert d.loss == pytest.approx(O.loss(st.theta, h, ts), rel=1e-10)
+
+
+def test_checkpoint_resume_is_bit_exact(G):
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T, K = 3000, 7, 200, 16
+    h, ts = make_problem(P, 1e-3, 1.0, 5)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=8)
+    with G.Gem(P, n) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 6)
+        g.sim_run(worker, tau, K)
+        straight = (g.theta(), g.S(), g.M())
+    with tempfile.TemporaryDirectory() as d:
+        path = os.path.join(d, "ck.bin")
+        with G.Gem(P, n) as g:
+            g.set_quadratic(h, ts, 0.01, 0.1, 6)
+            g.sim_run(worker[:77], tau[:77], K)
+            assert G.gem_save(g.h, path) == G.GEM_OK
+        with G.Gem(P, n) as g:
+            assert G.gem_load(g.h, path) == G.GEM_OK
+            assert g.clock == 77
+            g.sim_run(worker[77:], tau[77:], K)
+            resumed = (g.theta(), g.S(), g.M())
+        with G.Gem(P + 1, n) as g:
+            assert G.gem_load(g.h, path) == G.GEM_EIO
+    for a, b in zip(straight, resumed):
+        assert np.array_equal(a, b)
+
+
+def test_reset_worker_matches_oracle(G):
+    """A worker that fails and restarts: m_w = 0, it pulls theta now (Alg. 1 Worker start-up)."""
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n = 2000, 4
+    h, ts = make_problem(P, 1e-3, 1.0, 9)
+    worker, tau = G.gem_schedule_make(n, 100, G.GEM_LAW_EXP, seed=9)
+    st = O.State.initial(n, P)
+    ohp = O.Hyper(lr=0.01, sigma=0.1, momentum=0.9, seed=3)
+    with G.Gem(P, n) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 3)
+        g.sim_run(worker[:50], tau[:50], 8)
+        O.run(ohp, P, st, np.arange(P), h, ts, worker[:50], tau[:50])
+        assert G.gem_reset_worker(g.h, 2) == G.GEM_OK
+        st.S[2] = st.theta
+        st.M[2] = 0
+        st.pc[2] = st.t
+        w2 = worker[50:]
+        pc = st.pc.copy()
+        tau2 = []
+        for j, w in enumerate(w2):
+            tau2.append(st.t + j - pc[w])
+            pc[w] = st.t + j + 1
+        g.sim_run(w2, np.array(tau2, np.int32), 8)
+        O.run(ohp, P, st, np.arange(P), h, ts, w2, tau2)
+        _check((g.theta(), g.S(), g.M(), g.pull_clocks(), g.clock, None), st, "reset")
