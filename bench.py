@@ -1,0 +1,222 @@
+#!/usr/bin/env python3
+"""Benchmark of the GEM commit pipeline on one MI355X.
+
+One step is one simulated run of the workload's T commits: gem_sim_run plans
+the passes (validation, snapshot routing) and launches the fused
+stale-gradient + GEM-commit pass kernel once per K commits.  The schedule of
+the asynchronous system (which worker commits when, with what staleness) is
+the synthetic input: it is drawn by the library's host schedule generator
+before timing, for warmup + steps consecutive runs, so the system keeps
+running across steps.  The problem (h, theta*) is resident in HBM before the
+timed region.
+
+Prints one JSON line: parameter-commits/s (P x commits/s) and the fused
+pass's algorithmic HBM bandwidth against the 8 TB/s peak, with the CPU oracle
+timed on a bounded sample as a reported baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "parameter-commits/s (P×commits/s) + achieved HBM GB/s vs peak, P=25M n=100"
+KERNEL_SOURCES = ("gem_kernels.hip", "gem_device.hpp", "gem_internal.hpp")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "pass_kernel_headline_counters.md")
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_1805_08469_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per pass from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source for this workload; else None."""
+    if not os.path.exists(COUNTERS_FILE):
+        return None
+    text = open(COUNTERS_FILE).read()
+    m = re.search(r"```json\s*(\{.*?\})\s*```", text, flags=re.S)
+    if not m:
+        return None
+    d = json.loads(m.group(1))
+    if d.get("kernel_hash") != kernel_hash() or d.get("workload") != workload:
+        return None
+    return d.get("hbm_bytes_per_pass")
+
+
+def cpu_baseline(wl, h, ts, worker, tau, sample_elems: int, sample_commits: int):
+    """The oracle (single-threaded C, as it stands) on the first sample_commits
+    commits of the same schedule over the first sample_elems parameters."""
+    import numpy as np
+    import oracle as O
+
+    idx = np.arange(sample_elems, dtype=np.int64)
+    hp = O.Hyper(lr=wl.lr, sigma=wl.sigma, momentum=wl.momentum, bf16=wl.bf16, seed=wl.seed)
+    st = O.State.initial(wl.n, sample_elems)
+    t0 = time.perf_counter()
+    O.run(hp, wl.P, st, idx, h[:sample_elems], ts[:sample_elems], worker[:sample_commits],
+          tau[:sample_commits])
+    dt = time.perf_counter() - t0
+    return {
+        "value": sample_elems * sample_commits / dt,
+        "unit": "param-commits/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"first {sample_commits} commits of the {wl.name} schedule on parameters "
+                  f"0..{sample_elems - 1} ({dt:.1f} s, single thread)",
+    }
+
+
+def copy_ceiling(G, torch, nbytes: int, reps: int = 10) -> float:
+    """Device-to-device copy bandwidth (read + write bytes / time) of the
+    library's plain copy kernel, the practical HBM ceiling."""
+    n = nbytes // 4
+    src = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    G.gem_copy_f32(src.data_ptr(), dst.data_ptr(), n)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        assert G.gem_copy_f32(src.data_ptr(), dst.data_ptr(), n) == G.GEM_OK
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="headline",
+                    choices=["tiny", "small", "resnet18", "headline", "large"])
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle timing (profiling runs)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run the copy kernel (counter calibration) and exit")
+    ap.add_argument("--cpu-sample-elems", type=int, default=1 << 20)
+    ap.add_argument("--cpu-sample-commits", type=int, default=256)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the path shards by parameter index with no exchange per commit, but only the "
+              "one-GPU kernel is built and measured)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_1805_08469_amd import gem as G
+    from paper_1805_08469_amd.workloads import WORKLOADS, problem
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    torch.cuda.set_device(0)
+
+    if args.copy_probe:
+        gbs = copy_ceiling(G, torch, 1 << 30)
+        print(json.dumps({"copy_probe_bytes": 1 << 30, "copy_GBps": gbs}), flush=True)
+        return 0
+
+    wl = WORKLOADS[args.workload]
+    h, ts = problem(wl)
+    total = (args.warmup + args.steps) * wl.T
+    worker, tau = G.gem_schedule_make(wl.n, total, wl.law, wl.law_p0, wl.law_p1, seed=wl.seed)
+
+    stream = torch.cuda.current_stream()
+    g = G.Gem(wl.P, wl.n, stream=stream.cuda_stream)
+    g.set_quadratic(h, ts, wl.lr, wl.sigma, wl.seed, bf16=wl.bf16)
+    torch.cuda.synchronize()
+
+    def step(k):
+        sl = slice(k * wl.T, (k + 1) * wl.T)
+        g.sim_run(worker[sl], tau[sl], wl.K)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    G.gem_stats_reset(g.h)
+
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record(stream)
+    for k in range(args.warmup, args.warmup + args.steps):
+        step(k)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    gpu_s = e0.elapsed_time(e1) * 1e-3
+    stats = G.gem_stats(g.h)
+    assert stats.commits == args.steps * wl.T
+    g.close()
+
+    elapsed = max(gpu_s, 1e-12)
+    value = wl.P * stats.commits / elapsed
+    passes = stats.passes
+    alg_per_pass = stats.alg_bytes / passes
+    avg_pass_s = elapsed / passes
+    achieved = alg_per_pass / avg_pass_s / 1e9
+    traffic = measured_traffic(wl.name)
+
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "param-commits/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16-updates/f32" if wl.bf16 else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name, "P": wl.P, "n": wl.n, "commits_per_step": wl.T, "K": wl.K,
+            "sigma": wl.sigma, "lr": wl.lr, "momentum": wl.momentum,
+            "worker_law": {0: "exp", 1: "exp_uniform_mean", 2: "exp_lognormal_mean",
+                           3: "pareto"}[wl.law],
+            "passes_per_step": passes / args.steps,
+            "parallelism": "single-gpu",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "alg_bytes_per_launch": alg_per_pass,
+            "avg_launch_ms": avg_pass_s * 1e3,
+            "kernel": "pass_kernel<Generated, fast>",
+        },
+        "wall_s": wall,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, h, ts, worker, tau, min(args.cpu_sample_elems, wl.P),
+                                              min(args.cpu_sample_commits, total))
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -117,51 +117,16 @@ int check_sequence(const gem_handle* g, const int32_t* worker, const int32_t* ta
     return GEM_OK;
 }
 
-// Routes for the first k commits of `worker`: a worker's first commit in the
-// pass reads its rows from HBM, its last writes them back; in between its
-// pair lives in one register slot.  Returns false if more than kHeldSlots
-// workers would be held at once.
-bool assign_routes(const int32_t* worker, int k, uint8_t* routes)
-{
-    int32_t slot_worker[gemk::kHeldSlots] = {};
-    bool slot_busy[gemk::kHeldSlots] = {};
-    for (int j = 0; j < k; ++j) {
-        const int32_t w = worker[j];
-        int held = -1;
-        for (int s = 0; s < gemk::kHeldSlots; ++s)
-            if (slot_busy[s] && slot_worker[s] == w) held = s;
-        bool again = false;
-        for (int q = j + 1; q < k; ++q)
-            if (worker[q] == w) { again = true; break; }
-        uint8_t src = held >= 0 ? static_cast<uint8_t>(held) : gemk::kFromHbm;
-        uint8_t dst = gemk::kToHbm;
-        if (again) {
-            int s = held;
-            if (s < 0) {
-                for (int q = 0; q < gemk::kHeldSlots && s < 0; ++q)
-                    if (!slot_busy[q]) s = q;
-                if (s < 0) return false;
-                slot_busy[s] = true;
-                slot_worker[s] = w;
-            }
-            dst = static_cast<uint8_t>(s);
-        } else if (held >= 0) {
-            slot_busy[held] = false;
-        }
-        routes[j] = gemk::route(src, dst);
-    }
-    return true;
-}
-
 struct Pass {
     int32_t K = 0;
     int32_t worker[GEM_K_MAX];
     int32_t tau[GEM_K_MAX];
-    uint8_t routes[GEM_K_MAX];
+    uint32_t routes[GEM_K_MAX];
     int32_t distinct = 0;
 };
 
-// Cut a validated commit sequence into passes of at most Kmax commits.
+// Cut a validated commit sequence into passes of at most Kmax commits and
+// mark each commit whose worker also made the pass's previous commit.
 void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t Kmax,
                  std::vector<Pass>& out)
 {
@@ -169,9 +134,7 @@ void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t 
     int64_t j0 = 0;
     while (j0 < T) {
         Pass p;
-        int k = static_cast<int>(std::min<int64_t>(Kmax, T - j0));
-        while (k > 1 && !assign_routes(worker + j0, k, p.routes)) --k;
-        if (k == 1) assign_routes(worker + j0, 1, p.routes);
+        const int k = static_cast<int>(std::min<int64_t>(Kmax, T - j0));
         p.K = k;
         for (int j = 0; j < k; ++j) {
             const int32_t w = worker[j0 + j];
@@ -181,6 +144,7 @@ void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t 
             pc[w] = next_pull(g, t);
             bool seen = false;
             for (int q = 0; q < j; ++q) seen = seen || (p.worker[q] == w);
+            p.routes[j] = (j > 0 && p.worker[j - 1] == w) ? gemk::kRepeatOfPrevious : 0u;
             if (!seen) p.distinct += 1;
         }
         out.push_back(p);

@@ -8,16 +8,10 @@
 
 namespace gemk {
 
-// Per-commit source / destination of a worker's (snapshot, moment) pair inside
-// one fused pass.  A worker's first commit in the pass reads its rows from HBM;
-// a later commit of the same worker reads the pair its previous commit left in
-// a register slot.  A worker's last commit in the pass writes the rows back;
-// an earlier one leaves the pair in a slot.
-constexpr int kHeldSlots = 8;
-constexpr uint8_t kFromHbm = 0x0F;   // low nibble: source slot, or kFromHbm
-constexpr uint8_t kToHbm = 0x0F;     // high nibble: destination slot, or kToHbm
-
-inline uint8_t route(uint8_t src, uint8_t dst) { return static_cast<uint8_t>(src | (dst << 4)); }
+// Per-commit route flag of a fused pass: the committing worker also made the
+// pass's previous commit, so its current rows are that commit's output (the
+// prefetch issued before that commit's store holds stale rows).
+constexpr uint32_t kRepeatOfPrevious = 1u;
 
 // Runtime mode bits for the general kernel variant.
 enum : uint32_t {
@@ -47,7 +41,10 @@ struct PassArgs {
     int32_t pad_;
     int32_t worker[GEM_K_MAX];
     int32_t tau[GEM_K_MAX];  // staleness (adaptive-staleness rule only)
-    uint8_t routes[GEM_K_MAX];
+    // 32-bit so that a uniform per-commit read is a scalar load: gfx9 has no
+    // scalar byte load, and a vector one would wait on every outstanding
+    // memory operation of the wave.
+    uint32_t routes[GEM_K_MAX];
     const void* upd[GEM_K_MAX];  // caller updates (given-update variants)
 };
 

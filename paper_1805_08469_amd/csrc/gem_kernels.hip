@@ -3,9 +3,9 @@
 // The hot kernel is one fused pass: every thread owns four consecutive
 // parameters (one 16-byte chunk of every row) and applies the pass's K
 // commits to them in clock order.  theta, h and theta* are read once per
-// pass and theta written once; a committing worker's snapshot and moment rows
-// are read at its first commit in the pass and written at its last, the pair
-// living in registers in between.  Rows are read and written as 128-bit
+// pass and theta written once; each commit reads its worker's snapshot and
+// moment chunks (prefetched two commits ahead) and writes them back, so a
+// worker that commits twice in a pass re-reads what the same wavefront wrote.  Rows are read and written as 128-bit
 // accesses, consecutive lanes on consecutive chunks, so every wavefront moves
 // 1 KiB contiguous per row.  There is no contraction: the work is streaming
 // elementwise arithmetic (Philox, Box-Muller, the GEM step), bounded by HBM
@@ -121,111 +121,124 @@ __device__ __forceinline__ float4 load_given(const void* base, int64_t c, int64_
     }
 }
 
-struct Pair {
+struct Rows {
     float4 s, m;
 };
+
+__device__ __forceinline__ Rows load_rows(const PassArgs& a, int w, int64_t off)
+{
+    const int64_t row = static_cast<int64_t>(w) * a.Pp + off;
+    return Rows{*reinterpret_cast<const float4*>(a.S + row), *reinterpret_cast<const float4*>(a.M + row)};
+}
+
+__device__ __forceinline__ void store_rows(const PassArgs& a, int w, int64_t off, const Rows& r)
+{
+    const int64_t row = static_cast<int64_t>(w) * a.Pp + off;
+    *reinterpret_cast<float4*>(a.S + row) = r.s;
+    *reinterpret_cast<float4*>(a.M + row) = r.m;
+}
+
+// Per-thread context of a fused pass: the chunk, its central values and the
+// problem coefficients, kept in registers for the whole pass.
+struct Chunk {
+    int64_t c;       // chunk index (= Philox counter q of its four elements)
+    int64_t off;     // element offset 4c
+    bool active;
+    bool l0, l1, l2, l3;   // elements below the true length (diagnostics)
+    float4 th, hh, tt;
+};
+
+struct StepOut {
+    Rows out;    // the worker's (snapshot, moment) chunk after commit j
+    Rows next;   // rows prefetched for commit j + 2
+};
+
+// Commit j of a pass.  `rows` holds the committing worker's (snapshot, moment)
+// chunk, loaded two commits earlier, right after the store of commit j - 2.
+// Every commit writes its worker's chunk back before that prefetch, so the
+// prefetched rows are current unless the same worker committed at j - 1: then
+// they are taken from `prev`, that commit's output, still in registers.  Every
+// step issues exactly two loads and two stores, unconditionally, so the wait
+// for a step's rows never covers the loads issued after them.
+template <Source SRC, bool FAST, bool BF16, bool DIAG>
+__device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, int K, Chunk& ch, Rows rows,
+                                             const Rows& prev, DiagAcc& acc)
+{
+    const int w = a.worker[j];
+    if (a.routes[j] & kRepeatOfPrevious) rows = prev;
+
+    float4 d;
+    if (SRC == Source::Generated) {
+        const float4 z = normals4(static_cast<uint64_t>(ch.c), a.t0 + static_cast<uint32_t>(j),
+                                  a.key0, a.key1);
+        d.x = stale_update<BF16>(a.neg_lr, a.sigma, rows.s.x, ch.hh.x, ch.tt.x, z.x);
+        d.y = stale_update<BF16>(a.neg_lr, a.sigma, rows.s.y, ch.hh.y, ch.tt.y, z.y);
+        d.z = stale_update<BF16>(a.neg_lr, a.sigma, rows.s.z, ch.hh.z, ch.tt.z, z.z);
+        d.w = stale_update<BF16>(a.neg_lr, a.sigma, rows.s.w, ch.hh.w, ch.tt.w, z.w);
+    } else {
+        d = ch.active ? load_given<SRC>(a.upd[j], ch.c, a.P) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+
+    const int tau = a.tau[j];
+    StepOut r;
+    r.out.m = rows.m;
+    commit_element<FAST, DIAG>(a, tau, d.x, rows.s.x, ch.th.x, r.out.m.x, r.out.s.x, ch.active && ch.l0, acc);
+    commit_element<FAST, DIAG>(a, tau, d.y, rows.s.y, ch.th.y, r.out.m.y, r.out.s.y, ch.active && ch.l1, acc);
+    commit_element<FAST, DIAG>(a, tau, d.z, rows.s.z, ch.th.z, r.out.m.z, r.out.s.z, ch.active && ch.l2, acc);
+    commit_element<FAST, DIAG>(a, tau, d.w, rows.s.w, ch.th.w, r.out.m.w, r.out.s.w, ch.active && ch.l3, acc);
+    if (ch.active) {
+        store_rows(a, w, ch.off, r.out);
+        const int jn = j + 2 < K ? j + 2 : K - 1;   // past the end: a harmless in-bounds reload
+        r.next = load_rows(a, a.worker[jn], ch.off);
+    } else {
+        r.next = r.out;
+    }
+    return r;
+}
 
 template <Source SRC, bool FAST, bool BF16, bool DIAG>
 __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
 {
     const int64_t nchunk = a.Pp >> 2;
     const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    const bool active = c < nchunk;
-    if (!DIAG && !active) return;
-    const int64_t cc = active ? c : 0;   // inactive lanes (diagnostic variant) do no memory work
-
-    const int64_t off = cc * 4;
-    float4 th = make_float4(0.f, 0.f, 0.f, 0.f);
-    float4 hh = th, tt = th;
-    if (active) {
-        th = *reinterpret_cast<const float4*>(a.theta + off);
-        if (SRC == Source::Generated) {
-            hh = *reinterpret_cast<const float4*>(a.h + off);
-            tt = *reinterpret_cast<const float4*>(a.ts + off);
-        }
-    }
-
-    Pair held0, held1, held2, held3, held4, held5, held6, held7;
-    Pair next;
+    Chunk ch;
+    ch.active = c < nchunk;
+    if (!DIAG && !ch.active) return;
+    ch.c = ch.active ? c : 0;   // inactive lanes (diagnostic variant) do no memory work
+    ch.off = ch.c * 4;
+    ch.l0 = ch.off + 0 < a.P;
+    ch.l1 = ch.off + 1 < a.P;
+    ch.l2 = ch.off + 2 < a.P;
+    ch.l3 = ch.off + 3 < a.P;
+    ch.th = make_float4(0.f, 0.f, 0.f, 0.f);
+    ch.hh = ch.th;
+    ch.tt = ch.th;
     const int K = a.K;
-    if (active && (a.routes[0] & 0x0F) == kFromHbm) {
-        const int64_t row = static_cast<int64_t>(a.worker[0]) * a.Pp + off;
-        next.s = *reinterpret_cast<const float4*>(a.S + row);
-        next.m = *reinterpret_cast<const float4*>(a.M + row);
-    }
-
-    DiagAcc acc;
-    const bool l0 = off + 0 < a.P, l1 = off + 1 < a.P, l2 = off + 2 < a.P, l3 = off + 3 < a.P;
-
-    for (int j = 0; j < K; ++j) {
-        const uint32_t r = a.routes[j];
-        const uint32_t src = r & 0x0Fu;
-        const uint32_t dst = r >> 4;
-        const int w = a.worker[j];
-        Pair cur;
-        if (src == kFromHbm) {
-            cur = next;
-        } else {
-            switch (src) {
-            case 0: cur = held0; break;
-            case 1: cur = held1; break;
-            case 2: cur = held2; break;
-            case 3: cur = held3; break;
-            case 4: cur = held4; break;
-            case 5: cur = held5; break;
-            case 6: cur = held6; break;
-            default: cur = held7; break;
-            }
-        }
-        // Prefetch the next commit's rows if they come from HBM.  Such a row
-        // belongs to a worker not yet seen in this pass, so no store of this
-        // pass precedes it.
-        if (active && j + 1 < K && (a.routes[j + 1] & 0x0F) == kFromHbm) {
-            const int64_t row = static_cast<int64_t>(a.worker[j + 1]) * a.Pp + off;
-            next.s = *reinterpret_cast<const float4*>(a.S + row);
-            next.m = *reinterpret_cast<const float4*>(a.M + row);
-        }
-
-        float4 d;
+    Rows ring0{}, ring1{}, out0{}, out1{};
+    if (ch.active) {
+        ch.th = *reinterpret_cast<const float4*>(a.theta + ch.off);
         if (SRC == Source::Generated) {
-            const float4 z = normals4(static_cast<uint64_t>(cc), a.t0 + static_cast<uint32_t>(j),
-                                      a.key0, a.key1);
-            d.x = stale_update<BF16>(a.neg_lr, a.sigma, cur.s.x, hh.x, tt.x, z.x);
-            d.y = stale_update<BF16>(a.neg_lr, a.sigma, cur.s.y, hh.y, tt.y, z.y);
-            d.z = stale_update<BF16>(a.neg_lr, a.sigma, cur.s.z, hh.z, tt.z, z.z);
-            d.w = stale_update<BF16>(a.neg_lr, a.sigma, cur.s.w, hh.w, tt.w, z.w);
-        } else {
-            d = active ? load_given<SRC>(a.upd[j], cc, a.P) : make_float4(0.f, 0.f, 0.f, 0.f);
+            ch.hh = *reinterpret_cast<const float4*>(a.h + ch.off);
+            ch.tt = *reinterpret_cast<const float4*>(a.ts + ch.off);
         }
-
-        const int tau = a.tau[j];
-        Pair out;
-        out.m = cur.m;
-        commit_element<FAST, DIAG>(a, tau, d.x, cur.s.x, th.x, out.m.x, out.s.x, active && l0, acc);
-        commit_element<FAST, DIAG>(a, tau, d.y, cur.s.y, th.y, out.m.y, out.s.y, active && l1, acc);
-        commit_element<FAST, DIAG>(a, tau, d.z, cur.s.z, th.z, out.m.z, out.s.z, active && l2, acc);
-        commit_element<FAST, DIAG>(a, tau, d.w, cur.s.w, th.w, out.m.w, out.s.w, active && l3, acc);
-
-        if (dst == kToHbm) {
-            if (active) {
-                const int64_t row = static_cast<int64_t>(w) * a.Pp + off;
-                *reinterpret_cast<float4*>(a.S + row) = out.s;
-                *reinterpret_cast<float4*>(a.M + row) = out.m;
-            }
-        } else {
-            switch (dst) {
-            case 0: held0 = out; break;
-            case 1: held1 = out; break;
-            case 2: held2 = out; break;
-            case 3: held3 = out; break;
-            case 4: held4 = out; break;
-            case 5: held5 = out; break;
-            case 6: held6 = out; break;
-            default: held7 = out; break;
-            }
-        }
+        ring0 = load_rows(a, a.worker[0], ch.off);
+        ring1 = load_rows(a, a.worker[K > 1 ? 1 : 0], ch.off);
     }
-    if (active) *reinterpret_cast<float4*>(a.theta + off) = th;
+
+    // Two-entry ring unrolled by two: commit j reads ring[j mod 2] and refills
+    // it for commit j + 2, so no register copy of an in-flight load is needed.
+    DiagAcc acc;
+    int j = 0;
+    for (; j + 1 < K; j += 2) {
+        const StepOut s0 = pass_step<SRC, FAST, BF16, DIAG>(a, j, K, ch, ring0, out1, acc);
+        ring0 = s0.next;
+        out0 = s0.out;
+        const StepOut s1 = pass_step<SRC, FAST, BF16, DIAG>(a, j + 1, K, ch, ring1, out0, acc);
+        ring1 = s1.next;
+        out1 = s1.out;
+    }
+    if (j < K) (void)pass_step<SRC, FAST, BF16, DIAG>(a, j, K, ch, ring0, out1, acc);
+    if (ch.active) *reinterpret_cast<float4*>(a.theta + ch.off) = ch.th;
 
     if (DIAG) {
         __shared__ double red[4][kBlock];

@@ -1,8 +1,8 @@
 """GPU parity of whole simulated runs (gem_sim_run) against the oracle:
 theta, every worker's snapshot S[w] and moment M[w], element by element, on
 the same seeded schedules and noise.  Covers the tiny workload end to end,
-fusion of K commits per pass (with workers repeating inside a pass and passes
-cut for register pressure), ragged parameter counts, every commit-rule mode,
+fusion of K commits per pass (with workers repeating inside a pass at every
+distance), ragged parameter counts, every commit-rule mode,
 bfloat16 updates, diagnostics, checkpoint resume and worker restarts."""
 import os
 import tempfile
@@ -78,19 +78,42 @@ def test_fusion_is_invisible(G, K):
     worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=5)
     out, st = _run_both(G, P, n, worker, tau, K, _hp(G))
     _check(out, st, f"K={K}")
-    assert out[5].passes == -(-T // K)   # n = 3 never needs more than 3 held slots
+    assert out[5].passes == -(-T // K)
 
 
-def test_register_pressure_cuts_passes(G):
-    """Twelve workers in round robin keep up to 11 pairs in flight inside a
-    32-commit pass; the planner cuts passes so that at most 8 are held, and
-    the result is still the sequential one."""
-    P, n, T = 2048, 12, 240
-    worker = np.tile(np.arange(n, dtype=np.int32), T // n)
-    tau = np.array([t if t < n else n - 1 for t in range(T)], dtype=np.int32)
-    out, st = _run_both(G, P, n, worker, tau, 32, _hp(G))
-    _check(out, st, "round robin")
-    assert out[5].passes > -(-T // 32)
+def _taus(worker, n):
+    pc = np.zeros(n, dtype=np.int64)
+    tau = []
+    for t, w in enumerate(worker):
+        tau.append(t - pc[w])
+        pc[w] = t + 1
+    return np.array(tau, dtype=np.int32)
+
+
+@pytest.mark.parametrize("pattern", ["same_worker_runs", "distance_two", "round_robin_12",
+                                     "mixed"])
+@pytest.mark.parametrize("K", [2, 3, 32])
+def test_repeats_inside_a_pass(G, pattern, K):
+    """A worker that commits again inside a pass must see the snapshot and
+    moment its previous commit left: at distance 1 (taken from registers), at
+    distance 2 (re-read right after the store) and farther (re-read from
+    memory), with passes of every parity."""
+    rng = np.random.default_rng(K)
+    if pattern == "same_worker_runs":
+        worker = np.repeat(np.array([0, 1, 2, 1, 0, 3, 3, 2], np.int32), 5)
+        n = 4
+    elif pattern == "distance_two":
+        worker = np.tile(np.array([0, 1, 0, 1, 2, 3, 2, 3, 2], np.int32), 6)
+        n = 4
+    elif pattern == "round_robin_12":
+        n = 12
+        worker = np.tile(np.arange(n, dtype=np.int32), 20)
+    else:
+        n = 5
+        worker = rng.integers(0, n, size=200).astype(np.int32)
+    out, st = _run_both(G, 2048 + 5, n, worker, _taus(worker, n), K, _hp(G))
+    _check(out, st, pattern)
+    assert out[5].passes == -(-worker.size // K)
 
 
 @pytest.mark.parametrize("P", [1, 3, 63, 64, 65, 1000, 4133, 70001])
