@@ -30,6 +30,7 @@ struct gem_handle {
     float* h = nullptr;       // [Pp]
     float* ts = nullptr;      // [Pp]
     double* acc = nullptr;    // [5]: sum_ek, sum_proxy, n_clamped, n_elem_commits, loss
+    float* sink = nullptr;    // [2][kSinkChunks * 4] loads/stores a pass step does not need
     bool have_problem = false;
     gem_sim_params sp{};
     int64_t t = 0;
@@ -122,11 +123,66 @@ struct Pass {
     int32_t worker[GEM_K_MAX];
     int32_t tau[GEM_K_MAX];
     uint32_t routes[GEM_K_MAX];
-    int32_t distinct = 0;
+    int32_t distinct = 0;     // distinct workers (the algorithmic row traffic)
+    int32_t row_reads = 0;    // (snapshot, moment) row pairs the kernel reads
+    int32_t row_writes = 0;   // and writes
 };
 
-// Cut a validated commit sequence into passes of at most Kmax commits and
-// mark each commit whose worker also made the pass's previous commit.
+// Routes of one pass of k commits (see gem_internal.hpp).  A worker's chunk
+// is read from memory at its first commit in the pass and written back at its
+// last; in between it waits in one of kHeldSlots register slots.  When no slot
+// is free the chunk is written back and re-read: the prefetch of commit j + 2
+// is issued after the store of commit j, so it sees the stored values.  An
+// immediate repeat (the same worker at j and j + 1) cannot take that route --
+// the ring entry of commit j + 1 is loaded before commit j stores -- so if no
+// slot is free for it the pass has to end after commit j: the function then
+// returns j + 1 and the routes are not valid; otherwise it returns k.  reads
+// and writes count the row pairs that reach memory.
+int plan_routes(const int32_t* worker, int k, uint32_t* routes, int* reads, int* writes)
+{
+    int next[GEM_K_MAX];
+    for (int j = 0; j < k; ++j) {
+        next[j] = -1;
+        for (int q = j + 1; q < k; ++q)
+            if (worker[q] == worker[j]) { next[j] = q; break; }
+    }
+    int held_by[GEM_K_MAX];      // slot holding commit j's chunk, or -1
+    bool busy[gemk::kHeldSlots] = {};
+    uint32_t src[GEM_K_MAX], dst[GEM_K_MAX];
+    *reads = *writes = 0;
+    for (int j = 0; j < k; ++j) {
+        held_by[j] = -1;
+        int prev = -1;
+        for (int q = j - 1; q >= 0 && prev < 0; --q)
+            if (worker[q] == worker[j]) prev = q;
+        if (prev >= 0 && held_by[prev] >= 0) {
+            src[j] = static_cast<uint32_t>(held_by[prev]);
+            busy[held_by[prev]] = false;
+        } else {
+            src[j] = gemk::kFromRing;
+            *reads += 1;
+        }
+        dst[j] = gemk::kToMemory;
+        if (next[j] >= 0) {
+            for (int q = 0; q < gemk::kHeldSlots; ++q)
+                if (!busy[q]) {
+                    busy[q] = true;
+                    held_by[j] = q;
+                    dst[j] = static_cast<uint32_t>(q);
+                    break;
+                }
+            if (held_by[j] < 0 && next[j] == j + 1) return j + 1;
+        }
+        if (dst[j] == gemk::kToMemory) *writes += 1;
+    }
+    for (int j = 0; j < k; ++j) {
+        const bool pf = j + 2 < k && src[j + 2] == gemk::kFromRing;
+        routes[j] = gemk::make_route(src[j], dst[j], pf);
+    }
+    return k;
+}
+
+// Cut a validated commit sequence into passes of at most Kmax commits.
 void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t Kmax,
                  std::vector<Pass>& out)
 {
@@ -134,7 +190,10 @@ void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t 
     int64_t j0 = 0;
     while (j0 < T) {
         Pass p;
-        const int k = static_cast<int>(std::min<int64_t>(Kmax, T - j0));
+        int k = static_cast<int>(std::min<int64_t>(Kmax, T - j0));
+        // A shorter pass holds fewer workers at once, so this settles quickly.
+        for (int fit; (fit = plan_routes(worker + j0, k, p.routes, &p.row_reads, &p.row_writes)) < k;)
+            k = fit;
         p.K = k;
         for (int j = 0; j < k; ++j) {
             const int32_t w = worker[j0 + j];
@@ -144,7 +203,6 @@ void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t 
             pc[w] = next_pull(g, t);
             bool seen = false;
             for (int q = 0; q < j; ++q) seen = seen || (p.worker[q] == w);
-            p.routes[j] = (j > 0 && p.worker[j - 1] == w) ? gemk::kRepeatOfPrevious : 0u;
             if (!seen) p.distinct += 1;
         }
         out.push_back(p);
@@ -161,6 +219,9 @@ void base_args(const gem_handle* g, PassArgs& a)
     a.h = g->h;
     a.ts = g->ts;
     a.diag = g->acc;
+    a.sink_S = g->sink;
+    a.sink_M = g->sink + gemk::kSinkChunks * 4;
+    a.sink_mask = gemk::kSinkChunks - 1;
     a.Pp = g->Pp;
     a.P = g->P;
     a.key0 = static_cast<uint32_t>(g->sp.seed);
@@ -256,6 +317,7 @@ int gem_destroy(gem_t* g)
     (void)hipFree(g->h);
     (void)hipFree(g->ts);
     (void)hipFree(g->acc);
+    (void)hipFree(g->sink);
     delete g;
     return GEM_OK;
 }
@@ -294,6 +356,7 @@ int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, ge
         if (e == hipSuccess) e = hipMalloc(&g->S, tab);
         if (e == hipSuccess) e = hipMalloc(&g->M, tab);
         if (e == hipSuccess) e = hipMalloc(&g->acc, 8 * sizeof(double));
+        if (e == hipSuccess) e = hipMalloc(&g->sink, 2 * gemk::kSinkChunks * 4 * sizeof(float));
         if (e != hipSuccess) {
             note_hip_error("hipMalloc", e, __LINE__);
             (void)hipGetLastError();
@@ -306,6 +369,7 @@ int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, ge
         GEM_HIP(hipMemsetAsync(g->S, 0, tab, g->stream));
         GEM_HIP(hipMemsetAsync(g->M, 0, tab, g->stream));
         GEM_HIP(hipMemsetAsync(g->acc, 0, 8 * sizeof(double), g->stream));
+        GEM_HIP(hipMemsetAsync(g->sink, 0, 2 * gemk::kSinkChunks * 4 * sizeof(float), g->stream));
         GEM_HIP(hipStreamSynchronize(g->stream));
         return GEM_OK;
     }();

@@ -8,10 +8,26 @@
 
 namespace gemk {
 
-// Per-commit route flag of a fused pass: the committing worker also made the
-// pass's previous commit, so its current rows are that commit's output (the
-// prefetch issued before that commit's store holds stale rows).
-constexpr uint32_t kRepeatOfPrevious = 1u;
+// Per-commit route of a fused pass (host-planned, uniform across the grid).
+// Bits 0-3: where the committing worker's (snapshot, moment) chunk comes from:
+// a register slot 0..kHeldSlots-1 or the prefetch ring (memory).  Bits 4-7:
+// where it goes: a register slot or memory.  Bit 8: prefetch the rows of
+// commit j + 2, which reads them from memory.
+constexpr int kHeldSlots = 4;
+constexpr uint32_t kRouteSlotMask = 0xFu;
+constexpr uint32_t kRouteDstShift = 4;
+constexpr uint32_t kFromRing = 0xFu;
+constexpr uint32_t kToMemory = 0xFu;
+constexpr uint32_t kRoutePrefetch = 1u << 8;
+
+// Size of the sink rows, in 16-byte chunks (power of two); small enough to
+// stay resident in each XCD's L2.
+constexpr int64_t kSinkChunks = 4096;
+
+inline uint32_t make_route(uint32_t src, uint32_t dst, bool prefetch)
+{
+    return src | (dst << kRouteDstShift) | (prefetch ? kRoutePrefetch : 0u);
+}
 
 // Runtime mode bits for the general kernel variant.
 enum : uint32_t {
@@ -31,6 +47,9 @@ struct PassArgs {
     const float* h;          // [Pp]   (generated updates only)
     const float* ts;         // [Pp]   theta*
     double* diag;            // [4] accumulators (diagnostic variant only)
+    float* sink_S;           // [kSinkChunks * 4] target of loads/stores a step does not need
+    float* sink_M;
+    int64_t sink_mask;       // kSinkChunks - 1
     int64_t Pp;              // padded row length, a multiple of 64
     int64_t P;               // true length
     uint32_t key0, key1;     // noise seed

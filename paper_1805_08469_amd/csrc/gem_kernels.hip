@@ -3,9 +3,9 @@
 // The hot kernel is one fused pass: every thread owns four consecutive
 // parameters (one 16-byte chunk of every row) and applies the pass's K
 // commits to them in clock order.  theta, h and theta* are read once per
-// pass and theta written once; each commit reads its worker's snapshot and
-// moment chunks (prefetched two commits ahead) and writes them back, so a
-// worker that commits twice in a pass re-reads what the same wavefront wrote.  Rows are read and written as 128-bit
+// pass and theta written once; a worker's snapshot and moment chunks are
+// read (prefetched two commits ahead) at its first commit in the pass and
+// written at its last, held in registers in between.  Rows are read and written as 128-bit
 // accesses, consecutive lanes on consecutive chunks, so every wavefront moves
 // 1 KiB contiguous per row.  There is no contraction: the work is streaming
 // elementwise arithmetic (Philox, Box-Muller, the GEM step), bounded by HBM
@@ -131,12 +131,6 @@ __device__ __forceinline__ Rows load_rows(const PassArgs& a, int w, int64_t off)
     return Rows{*reinterpret_cast<const float4*>(a.S + row), *reinterpret_cast<const float4*>(a.M + row)};
 }
 
-__device__ __forceinline__ void store_rows(const PassArgs& a, int w, int64_t off, const Rows& r)
-{
-    const int64_t row = static_cast<int64_t>(w) * a.Pp + off;
-    *reinterpret_cast<float4*>(a.S + row) = r.s;
-    *reinterpret_cast<float4*>(a.M + row) = r.m;
-}
 
 // Per-thread context of a fused pass: the chunk, its central values and the
 // problem coefficients, kept in registers for the whole pass.
@@ -148,24 +142,58 @@ struct Chunk {
     float4 th, hh, tt;
 };
 
-struct StepOut {
-    Rows out;    // the worker's (snapshot, moment) chunk after commit j
-    Rows next;   // rows prefetched for commit j + 2
+// Register slots holding the (snapshot, moment) chunks of workers that commit
+// again later in the same pass.
+struct Held {
+    Rows h0, h1, h2, h3;
 };
 
-// Commit j of a pass.  `rows` holds the committing worker's (snapshot, moment)
-// chunk, loaded two commits earlier, right after the store of commit j - 2.
-// Every commit writes its worker's chunk back before that prefetch, so the
-// prefetched rows are current unless the same worker committed at j - 1: then
-// they are taken from `prev`, that commit's output, still in registers.  Every
-// step issues exactly two loads and two stores, unconditionally, so the wait
-// for a step's rows never covers the loads issued after them.
-template <Source SRC, bool FAST, bool BF16, bool DIAG>
-__device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, int K, Chunk& ch, Rows rows,
-                                             const Rows& prev, DiagAcc& acc)
+__device__ __forceinline__ Rows held_get(const Held& h, uint32_t slot)
 {
+    switch (slot) {
+    case 0: return h.h0;
+    case 1: return h.h1;
+    case 2: return h.h2;
+    default: return h.h3;
+    }
+}
+
+__device__ __forceinline__ Held held_put(Held h, uint32_t slot, const Rows& r)
+{
+    switch (slot) {
+    case 0: h.h0 = r; break;
+    case 1: h.h1 = r; break;
+    case 2: h.h2 = r; break;
+    default: h.h3 = r; break;
+    }
+    return h;
+}
+
+struct StepOut {
+    Rows out;    // the worker's (snapshot, moment) chunk after commit j
+    Rows next;   // ring entry for commit j + 2
+    Held held;
+};
+
+
+// Commit j of a pass.  The committing worker's (snapshot, moment) chunk comes
+// from the prefetch ring (loaded two commits earlier: a first commit in the
+// pass, or a worker whose earlier commit in the pass wrote its rows back) or
+// from a register slot.  After the commit the chunk is written back (the
+// worker's last commit in the pass, or no slot was free) or held in a slot;
+// the rows of commit j + 2 are prefetched if it reads them from memory.  Every step issues
+// one row-pair store and one row-pair load unconditionally -- those a step
+// does not need go to the small sink buffer, which stays in cache -- so the
+// wait for a step's rows never covers the loads issued after them.
+template <Source SRC, bool FAST, bool BF16, bool DIAG>
+__device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch, Rows ring,
+                                             Held held, DiagAcc& acc)
+{
+    const uint32_t route = a.routes[j];
+    const uint32_t src = route & kRouteSlotMask;
+    const uint32_t dst = (route >> kRouteDstShift) & kRouteSlotMask;
     const int w = a.worker[j];
-    if (a.routes[j] & kRepeatOfPrevious) rows = prev;
+    const Rows rows = src == kFromRing ? ring : held_get(held, src);
 
     float4 d;
     if (SRC == Source::Generated) {
@@ -186,12 +214,22 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, int K, Ch
     commit_element<FAST, DIAG>(a, tau, d.y, rows.s.y, ch.th.y, r.out.m.y, r.out.s.y, ch.active && ch.l1, acc);
     commit_element<FAST, DIAG>(a, tau, d.z, rows.s.z, ch.th.z, r.out.m.z, r.out.s.z, ch.active && ch.l2, acc);
     commit_element<FAST, DIAG>(a, tau, d.w, rows.s.w, ch.th.w, r.out.m.w, r.out.s.w, ch.active && ch.l3, acc);
+
+    if (dst != kToMemory) held = held_put(held, dst, r.out);
+    r.held = held;
     if (ch.active) {
-        store_rows(a, w, ch.off, r.out);
-        const int jn = j + 2 < K ? j + 2 : K - 1;   // past the end: a harmless in-bounds reload
-        r.next = load_rows(a, a.worker[jn], ch.off);
+        const int64_t sink_off = (ch.c & a.sink_mask) * 4;
+        const bool st = dst == kToMemory;
+        const int64_t so = st ? static_cast<int64_t>(w) * a.Pp + ch.off : sink_off;
+        *reinterpret_cast<float4*>((st ? a.S : a.sink_S) + so) = r.out.s;
+        *reinterpret_cast<float4*>((st ? a.M : a.sink_M) + so) = r.out.m;
+        const bool pf = (route & kRoutePrefetch) != 0;
+        const int64_t lo = pf ? static_cast<int64_t>(a.worker[j + 2 < a.K ? j + 2 : j]) * a.Pp + ch.off
+                              : sink_off;
+        r.next.s = *reinterpret_cast<const float4*>((pf ? a.S : a.sink_S) + lo);
+        r.next.m = *reinterpret_cast<const float4*>((pf ? a.M : a.sink_M) + lo);
     } else {
-        r.next = r.out;
+        r.next = ring;
     }
     return r;
 }
@@ -214,14 +252,15 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     ch.hh = ch.th;
     ch.tt = ch.th;
     const int K = a.K;
-    Rows ring0{}, ring1{}, out0{}, out1{};
+    Rows ring0{}, ring1{};
+    Held held{};
     if (ch.active) {
         ch.th = *reinterpret_cast<const float4*>(a.theta + ch.off);
         if (SRC == Source::Generated) {
             ch.hh = *reinterpret_cast<const float4*>(a.h + ch.off);
             ch.tt = *reinterpret_cast<const float4*>(a.ts + ch.off);
         }
-        ring0 = load_rows(a, a.worker[0], ch.off);
+        ring0 = load_rows(a, a.worker[0], ch.off);   // commit 0 always reads memory
         ring1 = load_rows(a, a.worker[K > 1 ? 1 : 0], ch.off);
     }
 
@@ -230,14 +269,13 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     DiagAcc acc;
     int j = 0;
     for (; j + 1 < K; j += 2) {
-        const StepOut s0 = pass_step<SRC, FAST, BF16, DIAG>(a, j, K, ch, ring0, out1, acc);
+        const StepOut s0 = pass_step<SRC, FAST, BF16, DIAG>(a, j, ch, ring0, held, acc);
         ring0 = s0.next;
-        out0 = s0.out;
-        const StepOut s1 = pass_step<SRC, FAST, BF16, DIAG>(a, j + 1, K, ch, ring1, out0, acc);
+        const StepOut s1 = pass_step<SRC, FAST, BF16, DIAG>(a, j + 1, ch, ring1, s0.held, acc);
         ring1 = s1.next;
-        out1 = s1.out;
+        held = s1.held;
     }
-    if (j < K) (void)pass_step<SRC, FAST, BF16, DIAG>(a, j, K, ch, ring0, out1, acc);
+    if (j < K) (void)pass_step<SRC, FAST, BF16, DIAG>(a, j, ch, ring0, held, acc);
     if (ch.active) *reinterpret_cast<float4*>(a.theta + ch.off) = ch.th;
 
     if (DIAG) {
