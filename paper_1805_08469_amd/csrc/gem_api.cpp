@@ -131,13 +131,12 @@ struct Pass {
 // Routes of one pass of k commits (see gem_internal.hpp).  A worker's chunk
 // is read from memory at its first commit in the pass and written back at its
 // last; in between it waits in one of kHeldSlots register slots.  When no slot
-// is free the chunk is written back and re-read: the prefetch of commit j + 2
-// is issued after the store of commit j, so it sees the stored values.  An
-// immediate repeat (the same worker at j and j + 1) cannot take that route --
-// the ring entry of commit j + 1 is loaded before commit j stores -- so if no
-// slot is free for it the pass has to end after commit j: the function then
-// returns j + 1 and the routes are not valid; otherwise it returns k.  reads
-// and writes count the row pairs that reach memory.
+// is free the chunk is written back and re-read, which is only valid if the
+// re-read is at least kPrefetchDepth commits later: the prefetch for commit
+// j + depth is issued right after commit j's store.  If a nearer repeat finds
+// no free slot the pass has to end after commit j: the function then returns
+// j + 1 and the routes are not valid; otherwise it returns k.  reads and
+// writes count the row pairs that reach memory.
 int plan_routes(const int32_t* worker, int k, uint32_t* routes, int* reads, int* writes)
 {
     int next[GEM_K_MAX];
@@ -171,12 +170,13 @@ int plan_routes(const int32_t* worker, int k, uint32_t* routes, int* reads, int*
                     dst[j] = static_cast<uint32_t>(q);
                     break;
                 }
-            if (held_by[j] < 0 && next[j] == j + 1) return j + 1;
+            if (held_by[j] < 0 && next[j] - j < gemk::kPrefetchDepth) return j + 1;
         }
         if (dst[j] == gemk::kToMemory) *writes += 1;
     }
     for (int j = 0; j < k; ++j) {
-        const bool pf = j + 2 < k && src[j + 2] == gemk::kFromRing;
+        const int jn = j + gemk::kPrefetchDepth;
+        const bool pf = jn < k && src[jn] == gemk::kFromRing;
         routes[j] = gemk::make_route(src[j], dst[j], pf);
     }
     return k;

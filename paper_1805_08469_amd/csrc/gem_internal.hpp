@@ -12,8 +12,10 @@ namespace gemk {
 // Bits 0-3: where the committing worker's (snapshot, moment) chunk comes from:
 // a register slot 0..kHeldSlots-1 or the prefetch ring (memory).  Bits 4-7:
 // where it goes: a register slot or memory.  Bit 8: prefetch the rows of
-// commit j + 2, which reads them from memory.
+// commit j + kPrefetchDepth, which reads them from memory.
 constexpr int kHeldSlots = 4;
+// How many commits ahead a step prefetches rows: the ring depth.
+constexpr int kPrefetchDepth = 2;
 constexpr uint32_t kRouteSlotMask = 0xFu;
 constexpr uint32_t kRouteDstShift = 4;
 constexpr uint32_t kFromRing = 0xFu;

@@ -171,20 +171,22 @@ __device__ __forceinline__ Held held_put(Held h, uint32_t slot, const Rows& r)
 
 struct StepOut {
     Rows out;    // the worker's (snapshot, moment) chunk after commit j
-    Rows next;   // ring entry for commit j + 2
+    Rows next;   // ring entry for commit j + kPrefetchDepth
     Held held;
 };
 
 
 // Commit j of a pass.  The committing worker's (snapshot, moment) chunk comes
-// from the prefetch ring (loaded two commits earlier: a first commit in the
-// pass, or a worker whose earlier commit in the pass wrote its rows back) or
-// from a register slot.  After the commit the chunk is written back (the
-// worker's last commit in the pass, or no slot was free) or held in a slot;
-// the rows of commit j + 2 are prefetched if it reads them from memory.  Every step issues
-// one row-pair store and one row-pair load unconditionally -- those a step
-// does not need go to the small sink buffer, which stays in cache -- so the
-// wait for a step's rows never covers the loads issued after them.
+// from the prefetch ring (loaded kPrefetchDepth commits earlier: a first
+// commit in the pass, or a worker whose earlier commit in the pass, at least
+// kPrefetchDepth commits back, wrote its rows back) or from a register slot.
+// After the commit the chunk is written back (the worker's last commit in the
+// pass, or no slot was free) or held in a slot; then the rows of commit
+// j + kPrefetchDepth are prefetched into the ring entry just consumed, if that
+// commit reads them from memory.  Every step issues one row-pair store and one
+// row-pair load unconditionally -- those a step does not need go to the small
+// sink buffer, which stays in cache -- so the wait for a step's rows never
+// covers the loads issued after them.
 template <Source SRC, bool FAST, bool BF16, bool DIAG>
 __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch, Rows ring,
                                              Held held, DiagAcc& acc)
@@ -224,8 +226,8 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
         *reinterpret_cast<float4*>((st ? a.S : a.sink_S) + so) = r.out.s;
         *reinterpret_cast<float4*>((st ? a.M : a.sink_M) + so) = r.out.m;
         const bool pf = (route & kRoutePrefetch) != 0;
-        const int64_t lo = pf ? static_cast<int64_t>(a.worker[j + 2 < a.K ? j + 2 : j]) * a.Pp + ch.off
-                              : sink_off;
+        const int jn = j + kPrefetchDepth < a.K ? j + kPrefetchDepth : j;
+        const int64_t lo = pf ? static_cast<int64_t>(a.worker[jn]) * a.Pp + ch.off : sink_off;
         r.next.s = *reinterpret_cast<const float4*>((pf ? a.S : a.sink_S) + lo);
         r.next.m = *reinterpret_cast<const float4*>((pf ? a.M : a.sink_M) + lo);
     } else {
@@ -252,7 +254,10 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     ch.hh = ch.th;
     ch.tt = ch.th;
     const int K = a.K;
-    Rows ring0{}, ring1{};
+    // Ring of prefetched rows, unrolled kPrefetchDepth ways so that every entry
+    // is a fixed set of registers: commit j reads ring[j mod depth] and refills
+    // it for commit j + depth -- no register copy of an in-flight load.
+    Rows ring[kPrefetchDepth];
     Held held{};
     if (ch.active) {
         ch.th = *reinterpret_cast<const float4*>(a.theta + ch.off);
@@ -260,22 +265,40 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
             ch.hh = *reinterpret_cast<const float4*>(a.h + ch.off);
             ch.tt = *reinterpret_cast<const float4*>(a.ts + ch.off);
         }
-        ring0 = load_rows(a, a.worker[0], ch.off);   // commit 0 always reads memory
-        ring1 = load_rows(a, a.worker[K > 1 ? 1 : 0], ch.off);
+        const int64_t sink_off = (ch.c & a.sink_mask) * 4;
+#pragma unroll
+        for (int u = 0; u < kPrefetchDepth; ++u) {
+            // Commit u reads memory iff it is the first commit of its worker
+            // (u < depth); the others prefetch from the sink.
+            const bool mem = u < K && (a.routes[u] & kRouteSlotMask) == kFromRing;
+            const int64_t lo = mem ? static_cast<int64_t>(a.worker[u]) * a.Pp + ch.off : sink_off;
+            ring[u].s = *reinterpret_cast<const float4*>((mem ? a.S : a.sink_S) + lo);
+            ring[u].m = *reinterpret_cast<const float4*>((mem ? a.M : a.sink_M) + lo);
+        }
+    } else {
+#pragma unroll
+        for (int u = 0; u < kPrefetchDepth; ++u) ring[u] = Rows{};
     }
 
-    // Two-entry ring unrolled by two: commit j reads ring[j mod 2] and refills
-    // it for commit j + 2, so no register copy of an in-flight load is needed.
     DiagAcc acc;
     int j = 0;
-    for (; j + 1 < K; j += 2) {
-        const StepOut s0 = pass_step<SRC, FAST, BF16, DIAG>(a, j, ch, ring0, held, acc);
-        ring0 = s0.next;
-        const StepOut s1 = pass_step<SRC, FAST, BF16, DIAG>(a, j + 1, ch, ring1, s0.held, acc);
-        ring1 = s1.next;
-        held = s1.held;
+    for (; j + kPrefetchDepth <= K; j += kPrefetchDepth) {
+#pragma unroll
+        for (int u = 0; u < kPrefetchDepth; ++u) {
+            const StepOut so = pass_step<SRC, FAST, BF16, DIAG>(a, j + u, ch, ring[u], held, acc);
+            ring[u] = so.next;
+            held = so.held;
+        }
     }
-    if (j < K) (void)pass_step<SRC, FAST, BF16, DIAG>(a, j, ch, ring0, held, acc);
+    // At most kPrefetchDepth - 1 commits remain.
+#pragma unroll
+    for (int u = 0; u + 1 < kPrefetchDepth; ++u) {
+        if (j + u < K) {
+            const StepOut so = pass_step<SRC, FAST, BF16, DIAG>(a, j + u, ch, ring[u], held, acc);
+            ring[u] = so.next;
+            held = so.held;
+        }
+    }
     if (ch.active) *reinterpret_cast<float4*>(a.theta + ch.off) = ch.th;
 
     if (DIAG) {

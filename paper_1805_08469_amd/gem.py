@@ -14,7 +14,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libgem.so")
+# The in-tree build; LIBGEM_PATH may name another build of the same sources.
+LIB_PATH = os.environ.get("LIBGEM_PATH") or os.path.join(_HERE, "libgem.so")
 
 GEM_OK, GEM_EINVAL, GEM_ENOMEM, GEM_EWORKER, GEM_ESTALE = 0, -1, -2, -3, -4
 GEM_EDTYPE, GEM_EHIP, GEM_ESTATE, GEM_EIO, GEM_EALIGN = -5, -6, -7, -8, -9
