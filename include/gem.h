@@ -57,6 +57,7 @@ enum { GEM_PI_CLAMP0 = 0, GEM_PI_LITERAL = 1 };            /* sign handling of p
 enum { GEM_KAPPA_LINEAR = 0, GEM_KAPPA_SQRT = 1 };         /* appendix B forms    */
 enum { GEM_PULL_POST_COMMIT = 0, GEM_PULL_PRE_COMMIT = 1 };/* when S[w] is taken  */
 enum { GEM_RULE_GEM = 0, GEM_RULE_DOWNPOUR = 1, GEM_RULE_ADAPTIVE = 2 };
+enum { GEM_PROXY_LOCAL = 0, GEM_PROXY_GLOBAL = 1 };        /* where m lives       */
 enum { GEM_LAW_EXP = 0, GEM_LAW_EXP_UNIFORM_MEAN = 1, GEM_LAW_EXP_LOGNORMAL_MEAN = 2,
        GEM_LAW_PARETO = 3 };
 enum { GEM_SNAPSHOT = 0, GEM_MOMENT = 1 };
@@ -73,7 +74,9 @@ typedef struct gem_handle gem_t;
  * workers' commits, eq. 2); PRE_COMMIT is Alg. 1's literal Worker order (pull,
  * commit, keep the pulled theta_t).  rule selects GEM or the two baselines of
  * Sec. 4: DOWNPOUR (commit dtheta unchanged, eq. 1) and adaptive staleness
- * (commit dtheta / (tau + 1)). */
+ * (commit dtheta / (tau + 1)).  proxy_mode LOCAL keeps one first moment per
+ * worker (Sec. 3.3); GLOBAL keeps one moment shared by all workers, refreshed
+ * by every commit (the global proxy of Sec. 6), stored as row 0 of M. */
 typedef struct {
     float momentum;
     float eps;
@@ -82,7 +85,7 @@ typedef struct {
     int32_t kappa_mode;
     int32_t pull_mode;
     int32_t rule;
-    int32_t reserved;
+    int32_t proxy_mode;
 } gem_hyperparams;
 
 /* Stale-gradient generator of the simulated workers: a worker whose snapshot
@@ -135,7 +138,7 @@ const char* gem_strerror(int code);
 const char* gem_last_error(void);
 
 /* Fill hp with Alg. 1's defaults: momentum 0.9, eps 1e-16, kappa 1, CLAMP0,
- * LINEAR, POST_COMMIT, GEM.  Returns GEM_EINVAL if hp is NULL. */
+ * LINEAR, POST_COMMIT, GEM, LOCAL.  Returns GEM_EINVAL if hp is NULL. */
 int gem_hyperparams_default(gem_hyperparams* hp);
 
 /* Create a master for P parameters and n workers on the current HIP device.
@@ -237,8 +240,9 @@ int gem_diag(gem_t* g, gem_diag_t* out);
 
 /* Work counters.  alg_bytes counts, per pass over P' (P padded to 64) elements:
  * theta read and written, h and theta* read (simulated runs), each distinct
- * worker's S and M rows read and written once, and caller updates read --
- * 4 bytes per float, 2 per bfloat16. */
+ * worker's S and M rows read and written once (GLOBAL proxy: its S row, plus
+ * the shared moment read and written once), and caller updates read -- 4
+ * bytes per float, 2 per bfloat16. */
 int gem_stats(gem_t* g, gem_stats_t* out);
 int gem_stats_reset(gem_t* g);
 

@@ -23,6 +23,7 @@ PI_CLAMP0, PI_LITERAL = 0, 1
 KAPPA_LINEAR, KAPPA_SQRT = 0, 1
 PULL_POST, PULL_PRE = 0, 1
 RULE_GEM, RULE_DOWNPOUR, RULE_ADAPTIVE = 0, 1, 2
+PROXY_LOCAL, PROXY_GLOBAL = 0, 1
 LAW_EXP, LAW_EXP_UNIFORM_MEAN, LAW_EXP_LOGNORMAL_MEAN, LAW_PARETO = 0, 1, 2, 3
 
 OK, EINVAL, ENOMEM, EWORKER, ESTALE = 0, -1, -2, -3, -4
@@ -42,6 +43,7 @@ class OracleConfig(C.Structure):
         ("pull_mode", C.c_int32),
         ("rule", C.c_int32),
         ("bf16", C.c_int32),
+        ("proxy", C.c_int32),
         ("seed", C.c_uint64),
     ]
 
@@ -223,13 +225,15 @@ class Hyper:
     pull_mode: int = PULL_POST
     rule: int = RULE_GEM
     bf16: bool = False
+    proxy: int = PROXY_LOCAL
     seed: int = 0
 
     def cfg(self, P: int, n: int) -> OracleConfig:
         return OracleConfig(P=P, n=n, lr=self.lr, sigma=self.sigma, momentum=self.momentum,
                             eps=self.eps, kappa=self.kappa, pi_mode=self.pi_mode,
                             kappa_mode=self.kappa_mode, pull_mode=self.pull_mode,
-                            rule=self.rule, bf16=int(self.bf16), seed=self.seed)
+                            rule=self.rule, bf16=int(self.bf16), proxy=self.proxy,
+                            seed=self.seed)
 
 
 class OracleError(RuntimeError):

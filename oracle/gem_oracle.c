@@ -34,8 +34,9 @@
  *     pull), so tau counts the other workers' commits in between and n=1
  *     means zero staleness; Alg. 1's literal pre-commit pull is a mode;
  *   - pi is clamped at zero (CLAMP0) unless the LITERAL mode is requested;
- *   - m is per worker; kappa enters as kappa*|m| (LINEAR, appendix B, last
- *     form) or sqrt(kappa)*|m| (SQRT, appendix B, first form).
+ *   - m is per worker (a global m is a mode); kappa enters as kappa*|m|
+ *     (LINEAR, appendix B, last form) or sqrt(kappa)*|m| (SQRT, appendix B,
+ *     first form).
  */
 #include <math.h>
 #include <stdint.h>
@@ -341,6 +342,11 @@ enum { OR_PI_CLAMP0 = 0, OR_PI_LITERAL = 1 };
 enum { OR_KAPPA_LINEAR = 0, OR_KAPPA_SQRT = 1 };
 enum { OR_RULE_GEM = 0, OR_RULE_DOWNPOUR = 1, OR_RULE_ADAPTIVE = 2 };
 enum { OR_OK = 0, OR_EINVAL = -1, OR_ENOMEM = -2, OR_EWORKER = -3, OR_ESTALE = -4 };
+/* Proxy estimate: each worker's own first moment (Sec. 3.3), or one moment
+ * shared by all workers and refreshed by every commit -- the global proxy the
+ * conclusion (Sec. 6) proposes as future work; it is then the velocity of
+ * sequential momentum SGD (eq. 14) driven by all the committed updates. */
+enum { OR_PROXY_LOCAL = 0, OR_PROXY_GLOBAL = 1 };
 
 typedef struct {
     int64_t P;        /* total parameter count; noise is keyed by global index */
@@ -355,6 +361,7 @@ typedef struct {
     int32_t pull_mode;
     int32_t rule;
     int32_t bf16;     /* round each update to bfloat16 before it is committed */
+    int32_t proxy;    /* OR_PROXY_LOCAL: m per worker; OR_PROXY_GLOBAL: one m in row 0 */
     uint64_t seed;
 } or_config;
 
@@ -458,9 +465,10 @@ int or_run(const or_config* c, const int64_t* idx, int64_t cnt,
         const int32_t tj = (int32_t)(t - pc[w]);
         or_commit_diag* dg = diag ? &diag[j] : NULL;
         if (dg) memset(dg, 0, sizeof(*dg));
+        const int64_t mrow = (c->proxy == OR_PROXY_GLOBAL) ? 0 : w;
         for (int64_t k = 0; k < cnt; ++k) {
             float* s_w = &S[(int64_t)w * cnt + k];
-            float* m_w = &M[(int64_t)w * cnt + k];
+            float* m_w = &M[mrow * cnt + k];
             const float s = *s_w;
             /* Stale gradient at the snapshot (notation table: dtheta = -eta grad L(s_t)). */
             float xi = or_normal(c->seed, (uint32_t)t, idx[k]);
@@ -498,11 +506,12 @@ int or_commit_given(const or_config* c, int64_t P, float* theta, float* S, float
         const int32_t tj = (int32_t)(t - pc[w]);
         or_commit_diag* dg = diag ? &diag[j] : NULL;
         if (dg) memset(dg, 0, sizeof(*dg));
+        const int64_t mrow = (c->proxy == OR_PROXY_GLOBAL) ? 0 : w;
         for (int64_t i = 0; i < P; ++i) {
             float di;
             if (d) di = d[j * P + i];
             else di = or_bits_to_float((uint32_t)db[j * P + i] << 16);
-            or_commit_element(c, k_eff, tj, di, &theta[i], &M[(int64_t)w * P + i],
+            or_commit_element(c, k_eff, tj, di, &theta[i], &M[mrow * P + i],
                               &S[(int64_t)w * P + i], dg,
                               trace ? &trace[(j * P + i) * 4] : NULL);
         }

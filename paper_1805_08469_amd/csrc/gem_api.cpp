@@ -68,6 +68,7 @@ bool valid_hp(const gem_hyperparams& hp)
     if (hp.pull_mode != GEM_PULL_POST_COMMIT && hp.pull_mode != GEM_PULL_PRE_COMMIT) return false;
     if (hp.rule != GEM_RULE_GEM && hp.rule != GEM_RULE_DOWNPOUR && hp.rule != GEM_RULE_ADAPTIVE)
         return false;
+    if (hp.proxy_mode != GEM_PROXY_LOCAL && hp.proxy_mode != GEM_PROXY_GLOBAL) return false;
     if (!std::isfinite(hp.momentum) || !std::isfinite(hp.eps) || !std::isfinite(hp.kappa))
         return false;
     if (hp.kappa_mode == GEM_KAPPA_SQRT && hp.kappa < 0.0f) return false;
@@ -83,7 +84,8 @@ float kappa_eff(const gem_hyperparams& hp)
 bool fast_rule(const gem_hyperparams& hp)
 {
     return hp.rule == GEM_RULE_GEM && hp.pi_mode == GEM_PI_CLAMP0 &&
-           hp.pull_mode == GEM_PULL_POST_COMMIT && kappa_eff(hp) == 1.0f;
+           hp.pull_mode == GEM_PULL_POST_COMMIT && hp.proxy_mode == GEM_PROXY_LOCAL &&
+           kappa_eff(hp) == 1.0f;
 }
 
 uint32_t mode_bits(const gem_hyperparams& hp)
@@ -94,6 +96,7 @@ uint32_t mode_bits(const gem_hyperparams& hp)
     if (hp.pull_mode == GEM_PULL_PRE_COMMIT) m |= gemk::kModePrePull;
     if (hp.rule == GEM_RULE_DOWNPOUR) m |= gemk::kModeDownpour;
     if (hp.rule == GEM_RULE_ADAPTIVE) m |= gemk::kModeAdaptive;
+    if (hp.proxy_mode == GEM_PROXY_GLOBAL) m |= gemk::kModeGlobalProxy;
     return m;
 }
 
@@ -249,7 +252,11 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
         std::memcpy(a.worker, p.worker, sizeof(p.worker));
         std::memcpy(a.tau, p.tau, sizeof(p.tau));
         std::memcpy(a.routes, p.routes, sizeof(p.routes));
-        double bytes = 2.0 * row_bytes + 4.0 * row_bytes * p.distinct;   // theta r+w, S/M r+w
+        // theta read and written; S and M rows of each distinct worker read and
+        // written (global proxy: S rows, and the shared moment once).
+        double bytes = g->hp.proxy_mode == GEM_PROXY_GLOBAL
+                           ? 4.0 * row_bytes + 2.0 * row_bytes * p.distinct
+                           : 2.0 * row_bytes + 4.0 * row_bytes * p.distinct;
         if (src == Source::Generated) {
             bytes += 2.0 * row_bytes;                                     // h, theta*
         } else {
@@ -304,6 +311,7 @@ int gem_hyperparams_default(gem_hyperparams* hp)
     hp->kappa_mode = GEM_KAPPA_LINEAR;
     hp->pull_mode = GEM_PULL_POST_COMMIT;
     hp->rule = GEM_RULE_GEM;
+    hp->proxy_mode = GEM_PROXY_LOCAL;
     return GEM_OK;
 }
 

@@ -38,6 +38,7 @@ enum : uint32_t {
     kModePrePull = 1u << 2,
     kModeDownpour = 1u << 3,
     kModeAdaptive = 1u << 4,
+    kModeGlobalProxy = 1u << 5,  // one moment (row 0 of M) shared by all workers
 };
 
 // Kernel argument block of one fused pass: K <= GEM_K_MAX commits at clocks

@@ -140,6 +140,7 @@ struct Chunk {
     bool active;
     bool l0, l1, l2, l3;   // elements below the true length (diagnostics)
     float4 th, hh, tt;
+    float4 mg;       // the shared moment (global proxy mode)
 };
 
 // Register slots holding the (snapshot, moment) chunks of workers that commit
@@ -195,7 +196,9 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     const uint32_t src = route & kRouteSlotMask;
     const uint32_t dst = (route >> kRouteDstShift) & kRouteSlotMask;
     const int w = a.worker[j];
-    const Rows rows = src == kFromRing ? ring : held_get(held, src);
+    Rows rows = src == kFromRing ? ring : held_get(held, src);
+    const bool global_m = !FAST && (a.mode & kModeGlobalProxy);
+    if (global_m) rows.m = ch.mg;   // the shared moment, carried like theta
 
     float4 d;
     if (SRC == Source::Generated) {
@@ -217,19 +220,24 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     commit_element<FAST, DIAG>(a, tau, d.z, rows.s.z, ch.th.z, r.out.m.z, r.out.s.z, ch.active && ch.l2, acc);
     commit_element<FAST, DIAG>(a, tau, d.w, rows.s.w, ch.th.w, r.out.m.w, r.out.s.w, ch.active && ch.l3, acc);
 
+    if (global_m) ch.mg = r.out.m;
     if (dst != kToMemory) held = held_put(held, dst, r.out);
     r.held = held;
     if (ch.active) {
+        // With the shared moment, only snapshot rows move; moment traffic goes
+        // to the sink.
         const int64_t sink_off = (ch.c & a.sink_mask) * 4;
         const bool st = dst == kToMemory;
         const int64_t so = st ? static_cast<int64_t>(w) * a.Pp + ch.off : sink_off;
+        const bool st_m = st && !global_m;
         *reinterpret_cast<float4*>((st ? a.S : a.sink_S) + so) = r.out.s;
-        *reinterpret_cast<float4*>((st ? a.M : a.sink_M) + so) = r.out.m;
+        *reinterpret_cast<float4*>((st_m ? a.M : a.sink_M) + (st_m ? so : sink_off)) = r.out.m;
         const bool pf = (route & kRoutePrefetch) != 0;
         const int jn = j + kPrefetchDepth < a.K ? j + kPrefetchDepth : j;
         const int64_t lo = pf ? static_cast<int64_t>(a.worker[jn]) * a.Pp + ch.off : sink_off;
+        const bool pf_m = pf && !global_m;
         r.next.s = *reinterpret_cast<const float4*>((pf ? a.S : a.sink_S) + lo);
-        r.next.m = *reinterpret_cast<const float4*>((pf ? a.M : a.sink_M) + lo);
+        r.next.m = *reinterpret_cast<const float4*>((pf_m ? a.M : a.sink_M) + (pf_m ? lo : sink_off));
     } else {
         r.next = ring;
     }
@@ -253,6 +261,9 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     ch.th = make_float4(0.f, 0.f, 0.f, 0.f);
     ch.hh = ch.th;
     ch.tt = ch.th;
+    ch.mg = ch.th;
+    const bool global_m = !FAST && (a.mode & kModeGlobalProxy);
+    if (global_m && ch.active) ch.mg = *reinterpret_cast<const float4*>(a.M + ch.off);
     const int K = a.K;
     // Ring of prefetched rows, unrolled kPrefetchDepth ways so that every entry
     // is a fixed set of registers: commit j reads ring[j mod depth] and refills
@@ -300,6 +311,7 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
         }
     }
     if (ch.active) *reinterpret_cast<float4*>(a.theta + ch.off) = ch.th;
+    if (global_m && ch.active) *reinterpret_cast<float4*>(a.M + ch.off) = ch.mg;
 
     if (DIAG) {
         __shared__ double red[4][kBlock];

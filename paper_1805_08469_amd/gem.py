@@ -24,6 +24,7 @@ GEM_PI_CLAMP0, GEM_PI_LITERAL = 0, 1
 GEM_KAPPA_LINEAR, GEM_KAPPA_SQRT = 0, 1
 GEM_PULL_POST_COMMIT, GEM_PULL_PRE_COMMIT = 0, 1
 GEM_RULE_GEM, GEM_RULE_DOWNPOUR, GEM_RULE_ADAPTIVE = 0, 1, 2
+GEM_PROXY_LOCAL, GEM_PROXY_GLOBAL = 0, 1
 GEM_LAW_EXP, GEM_LAW_EXP_UNIFORM_MEAN, GEM_LAW_EXP_LOGNORMAL_MEAN, GEM_LAW_PARETO = 0, 1, 2, 3
 GEM_SNAPSHOT, GEM_MOMENT = 0, 1
 GEM_K_MAX = 32
@@ -41,7 +42,7 @@ EXPORTED = (
 class gem_hyperparams(C.Structure):
     _fields_ = [("momentum", C.c_float), ("eps", C.c_float), ("kappa", C.c_float),
                 ("pi_mode", C.c_int32), ("kappa_mode", C.c_int32), ("pull_mode", C.c_int32),
-                ("rule", C.c_int32), ("reserved", C.c_int32)]
+                ("rule", C.c_int32), ("proxy_mode", C.c_int32)]
 
 
 class gem_sim_params(C.Structure):

@@ -89,6 +89,30 @@ def test_commit_batch(env, dtype, K):
     assert_parity("M", M, st.M)
 
 
+@pytest.mark.parametrize("K", [1, 32])
+def test_commit_batch_global_proxy(env, K):
+    """Caller updates committed with the shared moment (Sec. 6): row 0 of M."""
+    torch, G = env
+    P, n = 5003, 4
+    rng = np.random.default_rng(K + 100)
+    worker, tau = G.gem_schedule_make(n, 2 * K, G.GEM_LAW_EXP, seed=K + 1)
+    d = _updates(rng, 2 * K, P)
+    dev = _device_rows(torch, d)
+    hp = G.gem_hyperparams_default()
+    hp.proxy_mode = G.GEM_PROXY_GLOBAL
+    with G.Gem(P, n, hp) as g:
+        for b in range(2):
+            g.commit_batch([dev[j].data_ptr() for j in range(b * K, (b + 1) * K)], G.GEM_F32,
+                           worker[b * K:(b + 1) * K], tau[b * K:(b + 1) * K])
+        theta, S, M = g.theta(), g.S(), g.M()
+    st = O.State.initial(n, P)
+    O.commit_given(O.Hyper(proxy=O.PROXY_GLOBAL), st, worker, d, tau=tau)
+    assert_parity("theta", theta, st.theta)
+    assert_parity("S", S, st.S)
+    assert_parity("M", M, st.M)
+    assert np.all(M[1:] == 0)
+
+
 @pytest.mark.parametrize("bf16", [False, True])
 def test_generate_then_commit_equals_fused_run(env, bf16):
     """The unfused pipeline (generator kernel writes dtheta, commit kernel reads

@@ -25,17 +25,18 @@ def G():
     return gem
 
 
-def _hp(G, pi_mode=0, kappa=1.0, kappa_mode=0, pull=0, rule=0, momentum=0.9):
+def _hp(G, pi_mode=0, kappa=1.0, kappa_mode=0, pull=0, rule=0, momentum=0.9, proxy=0):
     hp = G.gem_hyperparams_default()
     hp.momentum, hp.kappa = momentum, kappa
     hp.pi_mode, hp.kappa_mode, hp.pull_mode, hp.rule = pi_mode, kappa_mode, pull, rule
+    hp.proxy_mode = proxy
     return hp
 
 
 def _ohp(hp, lr, sigma, seed, bf16=False):
     return O.Hyper(lr=lr, sigma=sigma, momentum=hp.momentum, eps=1e-16, kappa=hp.kappa,
                    pi_mode=hp.pi_mode, kappa_mode=hp.kappa_mode, pull_mode=hp.pull_mode,
-                   rule=hp.rule, bf16=bf16, seed=seed)
+                   rule=hp.rule, bf16=bf16, proxy=hp.proxy_mode, seed=seed)
 
 
 def _run_both(G, P, n, worker, tau, K, hp, lr=0.01, sigma=0.1, seed=7, bf16=False,
@@ -136,6 +137,8 @@ MODES = {
     "downpour": dict(rule=1),
     "adaptive": dict(rule=2),
     "mu0": dict(momentum=0.0),
+    "global_proxy": dict(proxy=1),
+    "global_proxy_kappa2_pre_pull": dict(proxy=1, kappa=2.0, pull=1),
 }
 
 

@@ -11,6 +11,8 @@
   pi converges (the reason for the CLAMP0 default).
 * Element independence: a run on an index subset equals the same entries of
   the full run (what the sampled parity tests at full size rely on).
+* The global proxy (Sec. 6): hand trace T3, and its exact reduction to the
+  per-worker proxy when there is one worker or no momentum.
 """
 import os
 
@@ -282,3 +284,58 @@ def test_modes_downpour_adaptive_pre_pull():
     O.commit_given(O.Hyper(rule=O.RULE_DOWNPOUR, pull_mode=O.PULL_PRE), st, [0, 1, 0], d,
                    tau=[0, 1, 2])
     assert st.S[0, 0] == 1.5 and st.S[1, 0] == 1.0
+
+
+def test_trace_T3_global_proxy():
+    rows = _rows("trace_T3_global.txt")
+    worker = [int(r[1]) for r in rows]
+    tau = [int(r[2]) for r in rows]
+    hp = O.Hyper(lr=0.5, sigma=0.0, momentum=0.5, proxy=O.PROXY_GLOBAL)
+    st = O.State.initial(2, 1)
+    snaps = []
+    for j in range(len(rows)):
+        snaps.append(float(st.S[worker[j], 0]))
+        O.run(hp, 1, st, [0], [1.0], [1.0], worker[j:j + 1], tau[j:j + 1])
+    st2 = O.State.initial(2, 1)
+    _, tr = O.run(hp, 1, st2, [0], [1.0], [1.0], worker, tau, trace=True)
+    for j, r in enumerate(rows):
+        s, d, m, a, pi, th = map(float, r[3:])
+        assert snaps[j] == s
+        assert (tr[j, 0, 2], tr[j, 0, 3], tr[j, 0, 0], tr[j, 0, 1]) == (d, m, a, pi)
+    assert st.theta[0] == float(rows[-1][-1]) == st2.theta[0]
+    assert st.M[0, 0] == float(rows[-1][5]) and st.M[1, 0] == 0.0   # one shared moment, in row 0
+
+
+@pytest.mark.parametrize("n,mu", [(1, 0.9), (5, 0.0)])
+def test_global_proxy_reduces_to_local(n, mu):
+    """With one worker, or with mu = 0 (m = dtheta), a shared moment and a
+    per-worker moment are the same quantity, so the runs agree bit for bit."""
+    P, T = 300, 120
+    h, ts = _quadratic(P, 11)
+    w, tau = O.schedule(n, T, O.LAW_EXP, 0, 0, seed=4)
+    out = []
+    for proxy in (O.PROXY_LOCAL, O.PROXY_GLOBAL):
+        hp = O.Hyper(lr=0.01, sigma=0.1, momentum=mu, proxy=proxy, seed=6)
+        st = O.State.initial(n, P)
+        O.run(hp, P, st, np.arange(P), h, ts, w, tau)
+        out.append(st)
+    assert np.array_equal(out[0].theta, out[1].theta)
+    assert np.array_equal(out[0].S, out[1].S)
+    if n == 1:
+        assert np.array_equal(out[0].M, out[1].M)
+
+
+def test_global_proxy_is_stable():
+    """Eq. 12 still holds step by step with the shared moment (the clamp does
+    not depend on where m comes from), and the tiny workload converges."""
+    from paper_1805_08469_amd.workloads import WORKLOADS
+    wl = WORKLOADS["tiny"]
+    h, ts = make_problem(wl.P, wl.h_lo, wl.h_hi, wl.seed)
+    w, tau = O.schedule(wl.n, 400, wl.law, seed=wl.seed)
+    hp = O.Hyper(lr=wl.lr, sigma=wl.sigma, momentum=wl.momentum, proxy=O.PROXY_GLOBAL, seed=1)
+    st = O.State.initial(wl.n, wl.P)
+    l0 = O.loss(st.theta, h, ts)
+    _, tr = O.run(hp, wl.P, st, np.arange(wl.P), h, ts, w, tau, trace=True)
+    a, pi, d, m = (tr[..., k].astype(np.float64) for k in range(4))
+    assert np.all(np.abs(a + pi * d) <= np.maximum(np.abs(m), np.abs(a)) * (1 + 4 * 2.0**-24))
+    assert O.loss(st.theta, h, ts) < 0.5 * l0
