@@ -56,14 +56,15 @@ def measured_traffic(workload: str):
     return d.get("hbm_bytes_per_pass")
 
 
-def cpu_baseline(wl, h, ts, worker, tau, sample_elems: int, sample_commits: int):
+def cpu_baseline(wl, h, ts, worker, tau, sample_elems: int, sample_commits: int, ghp):
     """The oracle (single-threaded C, as it stands) on the first sample_commits
     commits of the same schedule over the first sample_elems parameters."""
     import numpy as np
     import oracle as O
 
     idx = np.arange(sample_elems, dtype=np.int64)
-    hp = O.Hyper(lr=wl.lr, sigma=wl.sigma, momentum=wl.momentum, bf16=wl.bf16, seed=wl.seed)
+    hp = O.Hyper(lr=wl.lr, sigma=wl.sigma, momentum=wl.momentum, bf16=wl.bf16, seed=wl.seed,
+                 kappa=ghp.kappa, pi_mode=ghp.pi_mode, rule=ghp.rule, proxy=ghp.proxy_mode)
     st = O.State.initial(wl.n, sample_elems)
     t0 = time.perf_counter()
     O.run(hp, wl.P, st, idx, h[:sample_elems], ts[:sample_elems], worker[:sample_commits],
@@ -105,6 +106,11 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="headline",
                     choices=["tiny", "small", "resnet18", "headline", "large"])
+    ap.add_argument("--rule", default="gem", choices=["gem", "downpour", "adaptive"],
+                    help="commit rule (GEM, or the DOWNPOUR / adaptive-staleness baselines)")
+    ap.add_argument("--pi", default="clamp0", choices=["clamp0", "literal"])
+    ap.add_argument("--proxy", default="local", choices=["local", "global"])
+    ap.add_argument("--kappa", type=float, default=1.0)
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle timing (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -140,8 +146,16 @@ def main() -> int:
     total = (args.warmup + args.steps) * wl.T
     worker, tau = G.gem_schedule_make(wl.n, total, wl.law, wl.law_p0, wl.law_p1, seed=wl.seed)
 
+    hp = G.gem_hyperparams_default()
+    hp.rule = {"gem": G.GEM_RULE_GEM, "downpour": G.GEM_RULE_DOWNPOUR,
+               "adaptive": G.GEM_RULE_ADAPTIVE}[args.rule]
+    hp.pi_mode = G.GEM_PI_LITERAL if args.pi == "literal" else G.GEM_PI_CLAMP0
+    hp.proxy_mode = G.GEM_PROXY_GLOBAL if args.proxy == "global" else G.GEM_PROXY_LOCAL
+    hp.kappa = args.kappa
+    default_rule = (args.rule, args.pi, args.proxy, args.kappa) == ("gem", "clamp0", "local", 1.0)
+
     stream = torch.cuda.current_stream()
-    g = G.Gem(wl.P, wl.n, stream=stream.cuda_stream)
+    g = G.Gem(wl.P, wl.n, hp, stream=stream.cuda_stream)
     g.set_quadratic(h, ts, wl.lr, wl.sigma, wl.seed, bf16=wl.bf16)
     torch.cuda.synchronize()
 
@@ -175,7 +189,7 @@ def main() -> int:
     alg_per_pass = stats.alg_bytes / passes
     avg_pass_s = elapsed / passes
     achieved = alg_per_pass / avg_pass_s / 1e9
-    traffic = measured_traffic(wl.name)
+    traffic = measured_traffic(wl.name) if default_rule else None
 
     result = {
         "metric": METRIC,
@@ -196,6 +210,7 @@ def main() -> int:
             "worker_law": {0: "exp", 1: "exp_uniform_mean", 2: "exp_lognormal_mean",
                            3: "pareto"}[wl.law],
             "passes_per_step": passes / args.steps,
+            "rule": args.rule, "pi": args.pi, "proxy": args.proxy, "kappa": args.kappa,
             "parallelism": "single-gpu",
         },
         "roofline": {
@@ -207,13 +222,13 @@ def main() -> int:
             "traffic": traffic,
             "alg_bytes_per_launch": alg_per_pass,
             "avg_launch_ms": avg_pass_s * 1e3,
-            "kernel": "pass_kernel<Generated, fast>",
+            "kernel": "pass_kernel<Generated, %s>" % ("fast" if default_rule else "general"),
         },
         "wall_s": wall,
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, h, ts, worker, tau, min(args.cpu_sample_elems, wl.P),
-                                              min(args.cpu_sample_commits, total))
+                                              min(args.cpu_sample_commits, total), hp)
     print(json.dumps(result), flush=True)
     return 0
 

@@ -27,6 +27,7 @@ PROXY_LOCAL, PROXY_GLOBAL = 0, 1
 LAW_EXP, LAW_EXP_UNIFORM_MEAN, LAW_EXP_LOGNORMAL_MEAN, LAW_PARETO = 0, 1, 2, 3
 
 OK, EINVAL, ENOMEM, EWORKER, ESTALE = 0, -1, -2, -3, -4
+PI_BINS = 643
 
 
 class OracleConfig(C.Structure):
@@ -91,11 +92,15 @@ def lib():
         L.or_run.restype = C.c_int
         L.or_run.argtypes = [C.POINTER(OracleConfig), i64p, C.c_int64, f32p, f32p,
                              f32p, f32p, f32p, i64p, C.c_int64, i32p, i32p, C.c_int64,
-                             C.c_void_p, f32p]
+                             C.c_void_p, f32p, C.POINTER(C.c_uint32)]
         L.or_commit_given.restype = C.c_int
         L.or_commit_given.argtypes = [C.POINTER(OracleConfig), C.c_int64, f32p, f32p, f32p,
                                       i64p, C.c_int64, i32p, i32p, C.c_int64, f32p,
-                                      C.POINTER(C.c_uint16), C.c_void_p, f32p]
+                                      C.POINTER(C.c_uint16), C.c_void_p, f32p,
+                                      C.POINTER(C.c_uint32)]
+        L.or_pi_bin.restype = C.c_int
+        L.or_pi_bin.argtypes = [C.c_float]
+        L.or_pi_bin_array.argtypes = [f32p, i32p, C.c_int64]
         L.or_loss.restype = C.c_double
         L.or_loss.argtypes = [f32p, f32p, f32p, C.c_int64]
         _lib = L
@@ -243,11 +248,13 @@ class OracleError(RuntimeError):
 
 
 def run(hp: Hyper, P: int, st: State, idx, h, ts, worker, tau=None,
-        diag: bool = False, trace: bool = False):
+        diag: bool = False, trace: bool = False, pi_hist: bool = False):
     """Simulated run of len(worker) commits on the element subset ``idx``.
 
     The state ``st`` (theta, S, M restricted to ``idx``) is updated in place.
-    Returns (diag array or None, trace array [T, cnt, 4] of (a, pi, d, m) or None).
+    Returns (diag array or None, trace array [T, cnt, 4] of (a, pi, d, m) or None),
+    plus the per-commit histograms of the applied scale factor [T, PI_BINS]
+    as a third item when ``pi_hist`` is set.
     """
     idx = np.ascontiguousarray(idx, dtype=np.int64)
     cnt = idx.size
@@ -262,17 +269,18 @@ def run(hp: Hyper, P: int, st: State, idx, h, ts, worker, tau=None,
     assert st.theta.size == cnt and st.S.shape == (n, cnt) and h.size == cnt and ts.size == cnt
     dg = np.zeros(T, dtype=COMMIT_DIAG_DTYPE) if diag else None
     tr = np.zeros((T, cnt, 4), dtype=np.float32) if trace else None
+    ph = np.zeros((T, PI_BINS), dtype=np.uint32) if pi_hist else None
     cfg = hp.cfg(P, n)
     rc = lib().or_run(C.byref(cfg), _ptr(idx, C.c_int64), cnt, _ptr(h, C.c_float),
                       _ptr(ts, C.c_float), _ptr(st.theta, C.c_float), _ptr(st.S, C.c_float),
                       _ptr(st.M, C.c_float), _ptr(st.pc, C.c_int64), st.t,
                       _ptr(worker, C.c_int32), _ptr(tau_a, C.c_int32), T,
                       dg.ctypes.data if dg is not None else None,
-                      _ptr(tr, C.c_float))
+                      _ptr(tr, C.c_float), _ptr(ph, C.c_uint32))
     if rc != 0:
         raise OracleError(rc)
     st.t += T
-    return dg, tr
+    return (dg, tr, ph) if pi_hist else (dg, tr)
 
 
 def commit_given(hp: Hyper, st: State, worker, d, tau=None, diag: bool = False,
@@ -300,7 +308,7 @@ def commit_given(hp: Hyper, st: State, worker, d, tau=None, diag: bool = False,
                                _ptr(st.M, C.c_float), _ptr(st.pc, C.c_int64), st.t,
                                _ptr(worker, C.c_int32), _ptr(tau_a, C.c_int32), K, df, db,
                                dg.ctypes.data if dg is not None else None,
-                               _ptr(tr, C.c_float))
+                               _ptr(tr, C.c_float), None)
     if rc != 0:
         raise OracleError(rc)
     st.t += K
@@ -314,3 +322,11 @@ def loss(theta, h, ts) -> float:
     ts = np.ascontiguousarray(ts, dtype=np.float32)
     return float(lib().or_loss(_ptr(theta, C.c_float), _ptr(h, C.c_float), _ptr(ts, C.c_float),
                                theta.size))
+
+
+def pi_bin(pi) -> np.ndarray:
+    """Histogram bin of each applied scale factor (see or_pi_bin)."""
+    pi = np.ascontiguousarray(pi, dtype=np.float32)
+    out = np.empty(pi.shape, dtype=np.int32)
+    lib().or_pi_bin_array(_ptr(pi, C.c_float), _ptr(out, C.c_int32), pi.size)
+    return out

@@ -365,6 +365,22 @@ typedef struct {
     uint64_t seed;
 } or_config;
 
+/* Histogram of the applied scale factor of one commit (the per-parameter pi
+ * whose median Sec. 4 follows over time).  Bin 0: pi <= 0 or NaN (clamped);
+ * bin 1: 0 < pi < 2^-20; bins 2 + 16 o + f for 2^(o-20) (1 + f/16) <= pi
+ * < 2^(o-20) (1 + (f+1)/16), o in [0, 40), f in [0, 16); bin 642: pi >= 2^20. */
+#define OR_PI_BINS 643
+
+int or_pi_bin(float pi)
+{
+    if (!(pi > 0.0f)) return 0;
+    uint32_t b = or_float_to_bits(pi);
+    int32_t octave = (int32_t)((b >> 23) & 0xFFu) - 127 + 20;
+    if (octave < 0) return 1;
+    if (octave >= 40) return OR_PI_BINS - 1;
+    return 2 + octave * 16 + (int32_t)((b >> 19) & 0xFu);
+}
+
 typedef struct {
     double sum_ek;        /* sum_i 1/2 (theta_{t+1} - s)^2      (eq. 11) */
     double sum_proxy;     /* sum_i 1/2 (k_eff m)^2              (eq. 22) */
@@ -383,7 +399,7 @@ static float or_k_eff(const or_config* c)
  * (a, pi, d, m). */
 static void or_commit_element(const or_config* c, float k_eff, int32_t tau, float d,
                               float* theta, float* m_w, float* s_w,
-                              or_commit_diag* dg, float* trace)
+                              or_commit_diag* dg, float* trace, uint32_t* hist)
 {
     float th = *theta;
     float s = *s_w;
@@ -391,7 +407,7 @@ static void or_commit_element(const or_config* c, float k_eff, int32_t tau, floa
     float m = fmaf(c->momentum, *m_w, d);
     /* theta_t - s_t: the collective drift since the worker's pull (eq. 16). */
     float a = th - s;
-    float pi_raw = 0.0f, pi = 0.0f, psi;
+    float pi_raw = 0.0f, pi = 0.0f, psi, scale;
     if (c->rule == OR_RULE_GEM) {
         /* Alg. 1, second line, with kappa per appendix B. */
         float num = k_eff * fabsf(m) - fabsf(a);
@@ -401,12 +417,16 @@ static void or_commit_element(const or_config* c, float k_eff, int32_t tau, floa
         else pi = pi_raw;
         /* Alg. 1, third line, and eq. (3). */
         th = fmaf(pi, d, th);
+        scale = pi;
     } else if (c->rule == OR_RULE_DOWNPOUR) {
         th = th + d;                                   /* eq. (1) */
+        scale = 1.0f;
     } else {
         psi = d / (float)(tau + 1);                    /* dtheta / (tau + 1) */
         th = th + psi;
+        scale = 1.0f / (float)(tau + 1);
     }
+    if (hist) hist[or_pi_bin(scale)] += 1u;
     if (dg) {
         double e = (double)th - (double)s;
         double km = (double)k_eff * (double)m;
@@ -446,13 +466,14 @@ static int or_check_schedule(const or_config* c, const int64_t* pc_in, int64_t t
  * idx[0..cnt).  For commit j the worker is w = worker[j]; its update is
  * computed at its snapshot: dtheta = -eta (h (s - theta*) + sigma xi(seed, t, i)).
  * State arrays: theta[cnt], S[n*cnt], M[n*cnt] (row w at w*cnt), pc[n].
- * diag, if given, has T entries; trace, if given, has T*cnt*4 floats.
+ * diag, if given, has T entries; trace, if given, has T*cnt*4 floats;
+ * pi_hist, if given, has T*OR_PI_BINS counts (added to).
  */
 int or_run(const or_config* c, const int64_t* idx, int64_t cnt,
            const float* h, const float* ts,
            float* theta, float* S, float* M, int64_t* pc, int64_t t0,
            const int32_t* worker, const int32_t* tau, int64_t T,
-           or_commit_diag* diag, float* trace)
+           or_commit_diag* diag, float* trace, uint32_t* pi_hist)
 {
     if (!c || c->n <= 0 || cnt < 0 || T < 0) return OR_EINVAL;
     int rc = or_check_schedule(c, pc, t0, worker, tau, T);
@@ -478,7 +499,8 @@ int or_run(const or_config* c, const int64_t* idx, int64_t cnt,
             float d = neg_lr * g;
             if (c->bf16) d = or_round_bf16(d);
             or_commit_element(c, k_eff, tj, d, &theta[k], m_w, s_w, dg,
-                              trace ? &trace[(j * cnt + k) * 4] : NULL);
+                              trace ? &trace[(j * cnt + k) * 4] : NULL,
+                              pi_hist ? &pi_hist[j * OR_PI_BINS] : NULL);
         }
         pc[w] = (c->pull_mode == OR_PULL_PRE) ? t : t + 1;
     }
@@ -489,12 +511,12 @@ int or_run(const or_config* c, const int64_t* idx, int64_t cnt,
  * Commits of given updates (the gem_commit / gem_commit_batch semantics):
  * K commits starting at clock t0 on all P elements; update j is d[j*P ..]
  * (binary32) or db[j*P ..] (bfloat16 bit patterns) when d is NULL.
- * trace, if given, has K*P*4 floats (a, pi, d, m).
+ * trace, if given, has K*P*4 floats (a, pi, d, m); pi_hist as in or_run.
  */
 int or_commit_given(const or_config* c, int64_t P, float* theta, float* S, float* M,
                     int64_t* pc, int64_t t0, const int32_t* worker, const int32_t* tau,
                     int64_t K, const float* d, const uint16_t* db, or_commit_diag* diag,
-                    float* trace)
+                    float* trace, uint32_t* pi_hist)
 {
     if (!c || c->n <= 0 || P < 0 || K < 0 || (!d && !db)) return OR_EINVAL;
     int rc = or_check_schedule(c, pc, t0, worker, tau, K);
@@ -513,7 +535,8 @@ int or_commit_given(const or_config* c, int64_t P, float* theta, float* S, float
             else di = or_bits_to_float((uint32_t)db[j * P + i] << 16);
             or_commit_element(c, k_eff, tj, di, &theta[i], &M[mrow * P + i],
                               &S[(int64_t)w * P + i], dg,
-                              trace ? &trace[(j * P + i) * 4] : NULL);
+                              trace ? &trace[(j * P + i) * 4] : NULL,
+                              pi_hist ? &pi_hist[j * OR_PI_BINS] : NULL);
         }
         pc[w] = (c->pull_mode == OR_PULL_PRE) ? t : t + 1;
     }
@@ -552,4 +575,9 @@ void or_round_bf16_array(const float* x, float* out, int64_t n)
 void or_normals_at(uint64_t seed, uint32_t t, const int64_t* idx, int64_t count, float* out)
 {
     for (int64_t k = 0; k < count; ++k) out[k] = or_normal(seed, t, idx[k]);
+}
+
+void or_pi_bin_array(const float* pi, int32_t* out, int64_t n)
+{
+    for (int64_t k = 0; k < n; ++k) out[k] = or_pi_bin(pi[k]);
 }

@@ -13,6 +13,8 @@
   the full run (what the sampled parity tests at full size rely on).
 * The global proxy (Sec. 6): hand trace T3, and its exact reduction to the
   per-worker proxy when there is one worker or no momentum.
+* The per-commit histogram of scale factors: bins against their definition,
+  and the paper's observation that the factors shrink as workers are added.
 """
 import os
 
@@ -339,3 +341,69 @@ def test_global_proxy_is_stable():
     a, pi, d, m = (tr[..., k].astype(np.float64) for k in range(4))
     assert np.all(np.abs(a + pi * d) <= np.maximum(np.abs(m), np.abs(a)) * (1 + 4 * 2.0**-24))
     assert O.loss(st.theta, h, ts) < 0.5 * l0
+
+
+def _bin_by_frexp(x):
+    """The pi histogram bin from its definition, with float arithmetic:
+    2 + 16 o + f for 2^(o-20) (1 + f/16) <= x < 2^(o-20) (1 + (f+1)/16)."""
+    import math
+    if not (x > 0):
+        return 0
+    if math.isinf(x):
+        return O.PI_BINS - 1
+    mant, e = math.frexp(x)          # x = mant 2^e, mant in [0.5, 1)
+    octave = (e - 1) + 20
+    if octave < 0:
+        return 1
+    if octave >= 40:
+        return O.PI_BINS - 1
+    return 2 + 16 * octave + int((2 * mant - 1) * 16)
+
+
+def test_pi_bins_match_their_definition():
+    rng = np.random.default_rng(12)
+    xs = np.concatenate([np.exp(rng.uniform(np.log(1e-8), np.log(1e8), 20000)),
+                         [0.0, -0.0, -1.0, np.nan, np.inf, 2.0**-21, 2.0**-20, 1.0, 1.0625,
+                          2.0**20, 2.0**20 * (1 - 2**-24), 3e38]]).astype(np.float32)
+    got = O.pi_bin(xs)
+    want = np.array([_bin_by_frexp(float(x)) for x in xs])
+    assert np.array_equal(got, want)
+    assert list(got[-12:-7]) == [0, 0, 0, 0, O.PI_BINS - 1]          # 0, -0, <0, NaN, inf
+    assert list(got[-7:]) == [1, 2, 2 + 16 * 20, 3 + 16 * 20, O.PI_BINS - 1, O.PI_BINS - 2,
+                              O.PI_BINS - 1]
+
+
+def test_pi_histogram_counts_each_commits_factors():
+    P, n, T = 700, 6, 90
+    h, ts = _quadratic(P, 13)
+    w, tau = O.schedule(n, T, O.LAW_EXP, 0, 0, seed=3)
+    hp = O.Hyper(lr=0.01, sigma=0.1, momentum=0.9, seed=9)
+    st = O.State.initial(n, P)
+    _, tr, hist = O.run(hp, P, st, np.arange(P), h, ts, w, tau, trace=True, pi_hist=True)
+    assert hist.shape == (T, O.PI_BINS) and np.all(hist.sum(axis=1) == P)
+    for t in range(T):
+        assert np.array_equal(hist[t], np.bincount(O.pi_bin(tr[t, :, 1]), minlength=O.PI_BINS))
+
+
+def test_scale_factors_decrease_with_more_workers():
+    """Sec. 4: the per-parameter scale factors pi decrease as asynchronous
+    workers are added (more stale drift |theta - s| per commit).  On the tiny
+    problem's laws, over the second half of each run: the share of clamped
+    factors grows strictly with n and every quartile of the applied factor is
+    non-increasing, the median strictly so from n = 1 to 4."""
+    P, T = 2048, 1200
+    h, ts = _quadratic(P, 21)
+    quart, clamped = [], []
+    for n in (1, 2, 4, 16, 64):
+        w, tau = O.schedule(n, T, O.LAW_EXP, 0, 0, seed=n)
+        hp = O.Hyper(lr=0.01, sigma=0.1, momentum=0.9, seed=5)
+        st = O.State.initial(n, P)
+        _, _, hist = O.run(hp, P, st, np.arange(P), h, ts, w, tau, pi_hist=True)
+        H = hist[T // 2:].sum(axis=0).astype(np.int64)
+        c = np.cumsum(H)
+        quart.append([int(np.searchsorted(c, f * c[-1])) for f in (0.25, 0.5, 0.75)])
+        clamped.append(H[0] / H.sum())
+    assert all(a < b for a, b in zip(clamped, clamped[1:]))
+    for k in range(3):
+        assert all(a[k] >= b[k] for a, b in zip(quart, quart[1:]))
+    assert quart[0][1] > quart[1][1] > quart[2][1]
