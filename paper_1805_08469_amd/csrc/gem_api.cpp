@@ -37,6 +37,10 @@ struct gem_handle {
     std::vector<int64_t> pc;  // pull clock of each worker
     bool diag_on = false;
     int64_t diag_commits = 0;
+    uint32_t* pi_hist = nullptr;   // [hist_cap][GEM_PI_BINS] device counts
+    int64_t hist_cap = 0;
+    int64_t hist_count = 0;        // commits recorded so far (may exceed hist_cap)
+    bool hist_on = false;
     gem_stats_t stats{};
 };
 
@@ -263,7 +267,13 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
             for (int j = 0; j < p.K; ++j) a.upd[j] = upd[j0 + j];
             bytes += (src == Source::GivenBF16 ? 0.5 : 1.0) * row_bytes * p.K;
         }
-        GEM_HIP(gemk::launch_pass(a, src, fast, bf16_out, g->diag_on, g->stream));
+        const bool hist = g->hist_on && g->hist_count < g->hist_cap;
+        a.pi_hist = hist ? g->pi_hist : nullptr;
+        a.diag = g->diag_on ? g->acc : nullptr;
+        a.hist_first = g->hist_count;
+        a.hist_cap = g->hist_cap;
+        GEM_HIP(gemk::launch_pass(a, src, fast, bf16_out, g->diag_on || hist, g->stream));
+        if (g->hist_on) g->hist_count += p.K;
         for (int j = 0; j < p.K; ++j) g->pc[p.worker[j]] = next_pull(g, g->t + j);
         g->t += p.K;
         j0 += p.K;
@@ -326,6 +336,7 @@ int gem_destroy(gem_t* g)
     (void)hipFree(g->ts);
     (void)hipFree(g->acc);
     (void)hipFree(g->sink);
+    (void)hipFree(g->pi_hist);
     delete g;
     return GEM_OK;
 }
@@ -610,6 +621,43 @@ int gem_diag(gem_t* g, gem_diag_t* out)
     out->n_elem_commits = static_cast<int64_t>(host[3]);
     out->loss = host[4];
     out->n_commits = g->diag_commits;
+    return GEM_OK;
+}
+
+int gem_pi_hist_start(gem_t* g, int64_t capacity)
+{
+    if (!g || capacity < 1) return GEM_EINVAL;
+    const size_t bytes = static_cast<size_t>(capacity) * GEM_PI_BINS * sizeof(uint32_t);
+    if (capacity > g->hist_cap) {
+        GEM_HIP(hipStreamSynchronize(g->stream));
+        (void)hipFree(g->pi_hist);
+        g->pi_hist = nullptr;
+        g->hist_cap = 0;
+        if (hipMalloc(&g->pi_hist, bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            g->pi_hist = nullptr;
+            return GEM_ENOMEM;
+        }
+    }
+    GEM_HIP(hipMemsetAsync(g->pi_hist, 0, bytes, g->stream));
+    g->hist_cap = capacity;
+    g->hist_count = 0;
+    g->hist_on = true;
+    return GEM_OK;
+}
+
+int gem_pi_hist_read(gem_t* g, uint32_t* out, int64_t max_commits, int64_t* commits)
+{
+    if (!g || !commits || max_commits < 0 || (max_commits > 0 && !out)) return GEM_EINVAL;
+    if (!g->pi_hist) return GEM_ESTATE;
+    const int64_t recorded = std::min(g->hist_count, g->hist_cap);
+    const int64_t n = std::min(recorded, max_commits);
+    if (n > 0)
+        GEM_HIP(hipMemcpyAsync(out, g->pi_hist, static_cast<size_t>(n) * GEM_PI_BINS * sizeof(uint32_t),
+                               hipMemcpyDeviceToHost, g->stream));
+    GEM_HIP(hipStreamSynchronize(g->stream));
+    *commits = recorded;
+    g->hist_on = false;
     return GEM_OK;
 }
 

@@ -49,7 +49,10 @@ struct PassArgs {
     float* M;                // [n][Pp]
     const float* h;          // [Pp]   (generated updates only)
     const float* ts;         // [Pp]   theta*
-    double* diag;            // [4] accumulators (diagnostic variant only)
+    double* diag;            // [4] accumulators, or null (diagnostic variant only)
+    uint32_t* pi_hist;       // [hist_cap][GEM_PI_BINS] or null (diagnostic variant only)
+    int64_t hist_first;      // recording index of this pass's first commit
+    int64_t hist_cap;
     float* sink_S;           // [kSinkChunks * 4] target of loads/stores a step does not need
     float* sink_M;
     int64_t sink_mask;       // kSinkChunks - 1

@@ -24,7 +24,21 @@ constexpr int kBlock = 256;
 
 struct DiagAcc {
     double ek = 0.0, proxy = 0.0, clamped = 0.0, elems = 0.0;
+    uint32_t* hist = nullptr;   // block-local histogram of the current commit (LDS)
 };
+
+// Histogram bin of an applied scale factor, from its binary32 bits: 0 for
+// <= 0 or NaN, 1 below 2^-20, 16 bins per octave over [2^-20, 2^20), and the
+// last bin from 2^20 up.
+__device__ __forceinline__ int scale_bin(float x)
+{
+    if (!(x > 0.0f)) return 0;
+    const uint32_t b = __float_as_uint(x);
+    const int octave = static_cast<int>((b >> 23) & 0xFFu) - 107;
+    if (octave < 0) return 1;
+    if (octave >= 40) return GEM_PI_BINS - 1;
+    return 2 + octave * 16 + static_cast<int>((b >> 19) & 0xFu);
+}
 
 // One element of one commit.  th and m are the element's central value and
 // the committing worker's moment (in/out); s is its snapshot; d the update.
@@ -38,6 +52,7 @@ __device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float
     const float drift = th - s;                         // theta_t - s_t (eq. 16)
     float th_new;
     float pi_raw = 0.0f;
+    float scale;                                        // factor applied to dtheta
     bool gem_rule = true;
     if (FAST) {
         const float num = __builtin_fabsf(mn) - __builtin_fabsf(drift);
@@ -46,13 +61,16 @@ __device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float
         const float pi = (pi_raw > 0.0f) ? pi_raw : 0.0f;
         th_new = __builtin_fmaf(pi, d, th);             // eq. 3
         snap = th_new;
+        scale = pi;
     } else {
         if (a.mode & kModeDownpour) {
             gem_rule = false;
             th_new = th + d;                            // eq. 1
+            scale = 1.0f;
         } else if (a.mode & kModeAdaptive) {
             gem_rule = false;
             th_new = th + d / static_cast<float>(tau + 1);
+            scale = 1.0f / static_cast<float>(tau + 1);
         } else {
             const float km = (a.mode & kModeKappaMul) ? a.k_eff * __builtin_fabsf(mn)
                                                       : __builtin_fabsf(mn);
@@ -62,9 +80,11 @@ __device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float
             const float pi = (a.mode & kModeLiteralPi) ? pi_raw
                                                        : ((pi_raw > 0.0f) ? pi_raw : 0.0f);
             th_new = __builtin_fmaf(pi, d, th);
+            scale = pi;
         }
         snap = (a.mode & kModePrePull) ? th : th_new;
     }
+    if (DIAG && live && acc.hist) atomicAdd(&acc.hist[scale_bin(scale)], 1u);
     if (DIAG && live) {
         const double e = static_cast<double>(th_new) - static_cast<double>(s);
         const double kmd = static_cast<double>(FAST ? 1.0f : a.k_eff) * static_cast<double>(mn);
@@ -213,6 +233,14 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     }
 
     const int tau = a.tau[j];
+    // Diagnostic histogram of this commit's scale factors: every thread of
+    // the block is at commit j here (the loop is uniform), so the block-local
+    // histogram is cleared, filled and flushed between barriers.
+    const bool record = DIAG && acc.hist != nullptr && a.hist_first + j < a.hist_cap;
+    if (DIAG && acc.hist != nullptr) {
+        for (int b = threadIdx.x; b < GEM_PI_BINS; b += kBlock) acc.hist[b] = 0u;
+        __syncthreads();
+    }
     StepOut r;
     r.out.m = rows.m;
     commit_element<FAST, DIAG>(a, tau, d.x, rows.s.x, ch.th.x, r.out.m.x, r.out.s.x, ch.active && ch.l0, acc);
@@ -220,6 +248,15 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     commit_element<FAST, DIAG>(a, tau, d.z, rows.s.z, ch.th.z, r.out.m.z, r.out.s.z, ch.active && ch.l2, acc);
     commit_element<FAST, DIAG>(a, tau, d.w, rows.s.w, ch.th.w, r.out.m.w, r.out.s.w, ch.active && ch.l3, acc);
 
+    if (DIAG && acc.hist != nullptr) {
+        __syncthreads();
+        if (record) {
+            uint32_t* dst = a.pi_hist + (a.hist_first + j) * GEM_PI_BINS;
+            for (int b = threadIdx.x; b < GEM_PI_BINS; b += kBlock)
+                if (acc.hist[b]) atomicAdd(&dst[b], acc.hist[b]);
+        }
+        __syncthreads();
+    }
     if (global_m) ch.mg = r.out.m;
     if (dst != kToMemory) held = held_put(held, dst, r.out);
     r.held = held;
@@ -292,6 +329,10 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     }
 
     DiagAcc acc;
+    if constexpr (DIAG) {
+        __shared__ uint32_t hist_lds[GEM_PI_BINS];
+        if (a.pi_hist) acc.hist = hist_lds;
+    }
     int j = 0;
     for (; j + kPrefetchDepth <= K; j += kPrefetchDepth) {
 #pragma unroll
@@ -313,7 +354,7 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     if (ch.active) *reinterpret_cast<float4*>(a.theta + ch.off) = ch.th;
     if (global_m && ch.active) *reinterpret_cast<float4*>(a.M + ch.off) = ch.mg;
 
-    if (DIAG) {
+    if (DIAG && a.diag) {
         __shared__ double red[4][kBlock];
         red[0][threadIdx.x] = acc.ek;
         red[1][threadIdx.x] = acc.proxy;

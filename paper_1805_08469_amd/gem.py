@@ -28,6 +28,7 @@ GEM_PROXY_LOCAL, GEM_PROXY_GLOBAL = 0, 1
 GEM_LAW_EXP, GEM_LAW_EXP_UNIFORM_MEAN, GEM_LAW_EXP_LOGNORMAL_MEAN, GEM_LAW_PARETO = 0, 1, 2, 3
 GEM_SNAPSHOT, GEM_MOMENT = 0, 1
 GEM_K_MAX = 32
+GEM_PI_BINS = 643
 
 # Every symbol include/gem.h declares.
 EXPORTED = (
@@ -36,6 +37,7 @@ EXPORTED = (
     "gem_sim_run", "gem_read_theta", "gem_read_state", "gem_gather", "gem_clock",
     "gem_pull_clocks", "gem_reset_worker", "gem_diag_enable", "gem_diag_reset", "gem_diag",
     "gem_stats", "gem_stats_reset", "gem_save", "gem_load", "gem_sync", "gem_copy_f32",
+    "gem_pi_hist_start", "gem_pi_hist_read",
 )
 
 
@@ -115,6 +117,8 @@ def _load():
         "gem_load": (C.c_int, [vp, C.c_char_p]),
         "gem_sync": (C.c_int, [vp]),
         "gem_copy_f32": (C.c_int, [vp, vp, C.c_int64, vp]),
+        "gem_pi_hist_start": (C.c_int, [vp, C.c_int64]),
+        "gem_pi_hist_read": (C.c_int, [vp, C.POINTER(C.c_uint32), C.c_int64, i64p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -283,6 +287,17 @@ def gem_save(g: int, path: str) -> int:
 
 def gem_load(g: int, path: str) -> int:
     return _L.gem_load(g, path.encode())
+
+
+def gem_pi_hist_start(g: int, capacity: int) -> None:
+    _check(_L.gem_pi_hist_start(g, capacity), "gem_pi_hist_start")
+
+
+def gem_pi_hist_read(g: int, max_commits: int) -> np.ndarray:
+    out = np.zeros((max(max_commits, 0), GEM_PI_BINS), dtype=np.uint32)
+    n = C.c_int64()
+    _check(_L.gem_pi_hist_read(g, _p(out, C.c_uint32), max_commits, C.byref(n)), "gem_pi_hist_read")
+    return out[:min(n.value, max_commits)]
 
 
 def gem_sync(g: int) -> None:

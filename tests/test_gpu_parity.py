@@ -245,3 +245,30 @@ def test_reset_worker_matches_oracle(G):
         g.sim_run(w2, np.array(tau2, np.int32), 8)
         O.run(ohp, P, st, np.arange(P), h, ts, w2, tau2)
         _check((g.theta(), g.S(), g.M(), g.pull_clocks(), g.clock, None), st, "reset")
+
+
+@pytest.mark.parametrize("mode", ["default", "downpour", "adaptive", "literal", "global_proxy"])
+def test_pi_histograms_match_oracle(G, mode):
+    """Per-commit histograms of the applied scale factor (Sec. 4's per-parameter
+    pi), counted exactly; recorded alongside the energy diagnostics and cut
+    at the recording capacity."""
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T, K, cap = 6000 + 7, 5, 150, 16, 120
+    kw = {"default": {}, "downpour": dict(rule=1), "adaptive": dict(rule=2),
+          "literal": dict(pi_mode=1), "global_proxy": dict(proxy=1)}[mode]
+    hp = _hp(G, **kw)
+    h, ts = make_problem(P, 1e-3, 1.0, 3)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=7)
+    with G.Gem(P, n, hp) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 2)
+        G.gem_diag_enable(g.h, mode == "default")
+        G.gem_pi_hist_start(g.h, cap)
+        g.sim_run(worker, tau, K)
+        got = G.gem_pi_hist_read(g.h, T)
+        theta = g.theta()
+    st = O.State.initial(n, P)
+    _, _, hist = O.run(_ohp(hp, 0.01, 0.1, 2), P, st, np.arange(P), h, ts, worker, tau,
+                       pi_hist=True)
+    assert got.shape == (cap, G.GEM_PI_BINS)
+    assert np.array_equal(got, hist[:cap])
+    assert_parity("theta", theta, st.theta)
