@@ -153,6 +153,8 @@ def main() -> int:
     hp.proxy_mode = G.GEM_PROXY_GLOBAL if args.proxy == "global" else G.GEM_PROXY_LOCAL
     hp.kappa = args.kappa
     default_rule = (args.rule, args.pi, args.proxy, args.kappa) == ("gem", "clamp0", "local", 1.0)
+    variant = ("General" if (args.rule, args.pi, args.kappa) != ("gem", "clamp0", 1.0)
+               else "FastGlobal" if args.proxy == "global" else "Fast")
 
     stream = torch.cuda.current_stream()
     g = G.Gem(wl.P, wl.n, hp, stream=stream.cuda_stream)
@@ -168,20 +170,23 @@ def main() -> int:
     torch.cuda.synchronize()
     G.gem_stats_reset(g.h)
 
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    # One event at every step boundary, on the stream the passes run on: the
+    # first and last bracket the timed region, the others give per-step times.
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    e0.record(stream)
-    for k in range(args.warmup, args.warmup + args.steps):
-        step(k)
-    e1.record(stream)
+    ev[0].record(stream)
+    for k in range(args.steps):
+        step(args.warmup + k)
+        ev[k + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    gpu_s = e0.elapsed_time(e1) * 1e-3
+    gpu_s = ev[0].elapsed_time(ev[-1]) * 1e-3
+    step_ms = sorted(ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps))
     stats = G.gem_stats(g.h)
     assert stats.commits == args.steps * wl.T
     g.close()
+    copy_gbs = copy_ceiling(G, torch, 1 << 30)
 
     elapsed = max(gpu_s, 1e-12)
     value = wl.P * stats.commits / elapsed
@@ -199,6 +204,8 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": elapsed / args.steps * 1e3,
+        "step_ms": {"median": step_ms[len(step_ms) // 2], "min": step_ms[0],
+                    "max": step_ms[-1]},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -222,7 +229,9 @@ def main() -> int:
             "traffic": traffic,
             "alg_bytes_per_launch": alg_per_pass,
             "avg_launch_ms": avg_pass_s * 1e3,
-            "kernel": "pass_kernel<Generated, %s>" % ("fast" if default_rule else "general"),
+            "kernel": "pass_kernel<Generated, %s>" % variant,
+            "copy_ceiling_GBps": copy_gbs,
+            "frac_of_copy": achieved / copy_gbs,
         },
         "wall_s": wall,
     }

@@ -85,11 +85,14 @@ float kappa_eff(const gem_hyperparams& hp)
     return hp.kappa_mode == GEM_KAPPA_SQRT ? std::sqrt(hp.kappa) : hp.kappa;
 }
 
-bool fast_rule(const gem_hyperparams& hp)
+// The pass-kernel specialisation for these hyperparameters: the default rule
+// (GEM, CLAMP0, post-commit pull, kappa_eff = 1) has its own, for each proxy.
+gemk::Variant kernel_variant(const gem_hyperparams& hp)
 {
-    return hp.rule == GEM_RULE_GEM && hp.pi_mode == GEM_PI_CLAMP0 &&
-           hp.pull_mode == GEM_PULL_POST_COMMIT && hp.proxy_mode == GEM_PROXY_LOCAL &&
-           kappa_eff(hp) == 1.0f;
+    const bool default_rule = hp.rule == GEM_RULE_GEM && hp.pi_mode == GEM_PI_CLAMP0 &&
+                              hp.pull_mode == GEM_PULL_POST_COMMIT && kappa_eff(hp) == 1.0f;
+    if (!default_rule) return gemk::Variant::General;
+    return hp.proxy_mode == GEM_PROXY_GLOBAL ? gemk::Variant::FastGlobal : gemk::Variant::Fast;
 }
 
 uint32_t mode_bits(const gem_hyperparams& hp)
@@ -247,7 +250,7 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
 {
     PassArgs a;
     base_args(g, a);
-    const bool fast = fast_rule(g->hp);
+    const gemk::Variant variant = kernel_variant(g->hp);
     int64_t j0 = 0;
     const double row_bytes = 4.0 * static_cast<double>(g->Pp);
     for (const Pass& p : passes) {
@@ -272,7 +275,7 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
         a.diag = g->diag_on ? g->acc : nullptr;
         a.hist_first = g->hist_count;
         a.hist_cap = g->hist_cap;
-        GEM_HIP(gemk::launch_pass(a, src, fast, bf16_out, g->diag_on || hist, g->stream));
+        GEM_HIP(gemk::launch_pass(a, src, variant, bf16_out, g->diag_on || hist, g->stream));
         if (g->hist_on) g->hist_count += p.K;
         for (int j = 0; j < p.K; ++j) g->pc[p.worker[j]] = next_pull(g, g->t + j);
         g->t += p.K;

@@ -75,9 +75,13 @@ struct PassArgs {
 
 enum class Source { Generated = 0, GivenF32 = 1, GivenBF16 = 2 };
 
-// Launchers (defined in gem_kernels.hip).  `fast` selects the specialisation
-// for the default rule (GEM, CLAMP0, kappa_eff = 1, post-commit pull).
-hipError_t launch_pass(const PassArgs& a, Source src, bool fast, bool bf16_out, bool diag,
+// Pass-kernel specialisations.  Fast and FastGlobal take the default rule
+// (GEM, CLAMP0, kappa_eff = 1, post-commit pull) with per-worker or shared
+// first moments; General takes every mode as uniform runtime flags.
+enum class Variant { General = 0, Fast = 1, FastGlobal = 2 };
+
+// Launchers (defined in gem_kernels.hip).
+hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
                        hipStream_t stream);
 hipError_t launch_generate(const float* S_w, const float* h, const float* ts, void* out,
                            bool bf16, int64_t P, uint32_t t, uint32_t key0, uint32_t key1,

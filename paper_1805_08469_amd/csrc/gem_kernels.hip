@@ -208,7 +208,7 @@ struct StepOut {
 // row-pair load unconditionally -- those a step does not need go to the small
 // sink buffer, which stays in cache -- so the wait for a step's rows never
 // covers the loads issued after them.
-template <Source SRC, bool FAST, bool BF16, bool DIAG>
+template <Source SRC, Variant V, bool BF16, bool DIAG>
 __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch, Rows ring,
                                              Held held, DiagAcc& acc)
 {
@@ -217,7 +217,9 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     const uint32_t dst = (route >> kRouteDstShift) & kRouteSlotMask;
     const int w = a.worker[j];
     Rows rows = src == kFromRing ? ring : held_get(held, src);
-    const bool global_m = !FAST && (a.mode & kModeGlobalProxy);
+    constexpr bool FAST = V != Variant::General;
+    const bool global_m = V == Variant::FastGlobal ||
+                          (V == Variant::General && (a.mode & kModeGlobalProxy));
     if (global_m) rows.m = ch.mg;   // the shared moment, carried like theta
 
     float4 d;
@@ -281,7 +283,7 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     return r;
 }
 
-template <Source SRC, bool FAST, bool BF16, bool DIAG>
+template <Source SRC, Variant V, bool BF16, bool DIAG>
 __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
 {
     const int64_t nchunk = a.Pp >> 2;
@@ -299,7 +301,8 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     ch.hh = ch.th;
     ch.tt = ch.th;
     ch.mg = ch.th;
-    const bool global_m = !FAST && (a.mode & kModeGlobalProxy);
+    const bool global_m = V == Variant::FastGlobal ||
+                          (V == Variant::General && (a.mode & kModeGlobalProxy));
     if (global_m && ch.active) ch.mg = *reinterpret_cast<const float4*>(a.M + ch.off);
     const int K = a.K;
     // Ring of prefetched rows, unrolled kPrefetchDepth ways so that every entry
@@ -337,7 +340,7 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     for (; j + kPrefetchDepth <= K; j += kPrefetchDepth) {
 #pragma unroll
         for (int u = 0; u < kPrefetchDepth; ++u) {
-            const StepOut so = pass_step<SRC, FAST, BF16, DIAG>(a, j + u, ch, ring[u], held, acc);
+            const StepOut so = pass_step<SRC, V, BF16, DIAG>(a, j + u, ch, ring[u], held, acc);
             ring[u] = so.next;
             held = so.held;
         }
@@ -346,7 +349,7 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
 #pragma unroll
     for (int u = 0; u + 1 < kPrefetchDepth; ++u) {
         if (j + u < K) {
-            const StepOut so = pass_step<SRC, FAST, BF16, DIAG>(a, j + u, ch, ring[u], held, acc);
+            const StepOut so = pass_step<SRC, V, BF16, DIAG>(a, j + u, ch, ring[u], held, acc);
             ring[u] = so.next;
             held = so.held;
         }
@@ -467,34 +470,44 @@ inline unsigned blocks_for(int64_t items) {
     return static_cast<unsigned>((items + kBlock - 1) / kBlock);
 }
 
-template <Source SRC, bool FAST, bool BF16, bool DIAG>
+template <Source SRC, Variant V, bool BF16, bool DIAG>
 hipError_t launch_one(const PassArgs& a, hipStream_t st)
 {
-    hipLaunchKernelGGL((pass_kernel<SRC, FAST, BF16, DIAG>), dim3(blocks_for(a.Pp >> 2)),
+    hipLaunchKernelGGL((pass_kernel<SRC, V, BF16, DIAG>), dim3(blocks_for(a.Pp >> 2)),
                        dim3(kBlock), 0, st, a);
     return hipGetLastError();
 }
 
-template <Source SRC, bool BF16>
-hipError_t launch_fd(const PassArgs& a, bool fast, bool diag, hipStream_t st)
+template <Source SRC, Variant V, bool BF16>
+hipError_t launch_d(const PassArgs& a, bool diag, hipStream_t st)
 {
-    if (fast) return diag ? launch_one<SRC, true, BF16, true>(a, st) : launch_one<SRC, true, BF16, false>(a, st);
-    return diag ? launch_one<SRC, false, BF16, true>(a, st) : launch_one<SRC, false, BF16, false>(a, st);
+    return diag ? launch_one<SRC, V, BF16, true>(a, st) : launch_one<SRC, V, BF16, false>(a, st);
+}
+
+template <Source SRC, bool BF16>
+hipError_t launch_fd(const PassArgs& a, Variant v, bool diag, hipStream_t st)
+{
+    switch (v) {
+    case Variant::Fast: return launch_d<SRC, Variant::Fast, BF16>(a, diag, st);
+    case Variant::FastGlobal: return launch_d<SRC, Variant::FastGlobal, BF16>(a, diag, st);
+    case Variant::General: break;
+    }
+    return launch_d<SRC, Variant::General, BF16>(a, diag, st);
 }
 
 }  // namespace
 
-hipError_t launch_pass(const PassArgs& a, Source src, bool fast, bool bf16_out, bool diag,
+hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
                        hipStream_t stream)
 {
     switch (src) {
     case Source::Generated:
-        return bf16_out ? launch_fd<Source::Generated, true>(a, fast, diag, stream)
-                        : launch_fd<Source::Generated, false>(a, fast, diag, stream);
+        return bf16_out ? launch_fd<Source::Generated, true>(a, v, diag, stream)
+                        : launch_fd<Source::Generated, false>(a, v, diag, stream);
     case Source::GivenF32:
-        return launch_fd<Source::GivenF32, false>(a, fast, diag, stream);
+        return launch_fd<Source::GivenF32, false>(a, v, diag, stream);
     case Source::GivenBF16:
-        return launch_fd<Source::GivenBF16, false>(a, fast, diag, stream);
+        return launch_fd<Source::GivenBF16, false>(a, v, diag, stream);
     }
     return hipErrorInvalidValue;
 }

@@ -39,7 +39,7 @@ def _free_bytes():
     return free
 
 
-def _workload_parity(G, name, T=None):
+def _workload_parity(G, name, T=None, proxy=0):
     from paper_1805_08469_amd.workloads import WORKLOADS, problem
     wl = WORKLOADS[name]
     if T is not None:
@@ -50,15 +50,18 @@ def _workload_parity(G, name, T=None):
     h, ts = problem(wl)
     worker, tau = G.gem_schedule_make(wl.n, wl.T, wl.law, wl.law_p0, wl.law_p1, seed=wl.seed)
     idx = _sample(wl.P, seed=wl.P)
-    print(f"[{name}] P={wl.P} n={wl.n} T={wl.T} K={wl.K} bf16={wl.bf16} sample={idx.size}",
-          flush=True)
-    with G.Gem(wl.P, wl.n) as g:
+    print(f"[{name}] P={wl.P} n={wl.n} T={wl.T} K={wl.K} bf16={wl.bf16} proxy={proxy} "
+          f"sample={idx.size}", flush=True)
+    ghp = G.gem_hyperparams_default()
+    ghp.proxy_mode = proxy
+    with G.Gem(wl.P, wl.n, ghp) as g:
         g.set_quadratic(h, ts, wl.lr, wl.sigma, wl.seed, bf16=wl.bf16)
         g.sim_run(worker, tau, wl.K)
         theta, S, M = g.gather(idx)
         pc = g.pull_clocks()
         stats = g.stats()
-    hp = O.Hyper(lr=wl.lr, sigma=wl.sigma, momentum=wl.momentum, bf16=wl.bf16, seed=wl.seed)
+    hp = O.Hyper(lr=wl.lr, sigma=wl.sigma, momentum=wl.momentum, bf16=wl.bf16, seed=wl.seed,
+                 proxy=proxy)
     st = O.State.initial(wl.n, idx.size)
     O.run(hp, wl.P, st, idx, h[idx], ts[idx], worker, tau)
     assert np.array_equal(pc, st.pc)
@@ -80,6 +83,12 @@ def test_resnet18(G):
 def test_headline(G):
     s = _workload_parity(G, "headline")
     assert -(-5000 // 32) <= s.passes <= 1.1 * -(-5000 // 32)
+
+
+def test_headline_global_proxy(G):
+    """The shared-moment mode at the headline size, as bench.py --proxy global
+    runs it.  The shared moment is row 0 of M; the other rows stay zero."""
+    _workload_parity(G, "headline", proxy=1)
 
 
 def test_large(G):

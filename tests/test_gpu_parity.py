@@ -173,12 +173,13 @@ def test_literal_diverges_on_gpu_like_oracle(G):
     assert np.nanmax(np.abs(st.theta)) > 1e6
 
 
-def test_diagnostics_match_oracle(G):
+@pytest.mark.parametrize("proxy", [0, 1], ids=["local", "global"])
+def test_diagnostics_match_oracle(G, proxy):
     from paper_1805_08469_amd.workloads import make_problem
     P, n, T, K = 10_000 + 3, 8, 200, 8
     h, ts = make_problem(P, 1e-3, 1.0, 2)
     worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=2)
-    hp = _hp(G)
+    hp = _hp(G, proxy=proxy)
     with G.Gem(P, n, hp) as g:
         g.set_quadratic(h, ts, 0.01, 0.1, 4)
         G.gem_diag_enable(g.h, True)
