@@ -30,7 +30,12 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 METRIC = "parameter-commits/s (P×commits/s) + achieved HBM GB/s vs peak, P=25M n=100"
 KERNEL_SOURCES = ("gem_kernels.hip", "gem_device.hpp", "gem_internal.hpp")
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "pass_kernel_headline_counters.md")
+# Committed rocprofv3 counter summaries, per (workload, proxy) of the fast kernel variants.
+COUNTERS_FILES = {
+    ("headline", "local"): os.path.join(ROOT, "profiles", "pass_kernel_headline_counters.md"),
+    ("headline", "global"): os.path.join(ROOT, "profiles",
+                                         "pass_kernel_headline_global_proxy_counters.md"),
+}
 
 
 def kernel_hash() -> str:
@@ -41,17 +46,19 @@ def kernel_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, proxy: str):
     """HBM bytes per pass from the committed rocprofv3 counter summary, if it
     was taken on the current kernel source for this workload; else None."""
-    if not os.path.exists(COUNTERS_FILE):
+    path = COUNTERS_FILES.get((workload, proxy))
+    if path is None or not os.path.exists(path):
         return None
-    text = open(COUNTERS_FILE).read()
+    text = open(path).read()
     m = re.search(r"```json\s*(\{.*?\})\s*```", text, flags=re.S)
     if not m:
         return None
     d = json.loads(m.group(1))
-    if d.get("kernel_hash") != kernel_hash() or d.get("workload") != workload:
+    if (d.get("kernel_hash") != kernel_hash() or d.get("workload") != workload
+            or d.get("proxy", "local") != proxy):
         return None
     return d.get("hbm_bytes_per_pass")
 
@@ -99,6 +106,36 @@ def copy_ceiling(G, torch, nbytes: int, reps: int = 10) -> float:
     return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
+def compare_rules(G, P: int = 1 << 20, T: int = 3000, every: int = 500, K: int = 16):
+    """Loss per parameter, every `every` commits, of GEM (mu = 0.9), DOWNPOUR and
+    the adaptive-staleness rule (both mu = 0) on a synthetic diagonal quadratic
+    (h ~ LogUniform[1e-3, 1], theta* ~ N(0, 1), noise sigma = 0.1), for n = 1..30
+    exponential-time workers and a normal (0.01) and a misspecified (0.5)
+    learning rate: the experiments of Sec. 4 on stability and misspecification,
+    run through the library."""
+    from paper_1805_08469_amd.workloads import make_problem
+    h, ts = make_problem(P, 1e-3, 1.0, 31)
+    rules = {"gem": (G.GEM_RULE_GEM, 0.9), "downpour": (G.GEM_RULE_DOWNPOUR, 0.0),
+             "adaptive": (G.GEM_RULE_ADAPTIVE, 0.0)}
+    table = []
+    for lr in (0.01, 0.5):
+        for n in (1, 5, 10, 20, 30):
+            worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=n)
+            for name, (rule, mu) in rules.items():
+                hp = G.gem_hyperparams_default()
+                hp.rule, hp.momentum = rule, mu
+                curve = []
+                with G.Gem(P, n, hp) as g:
+                    g.set_quadratic(h, ts, lr, 0.1, 9)
+                    for c in range(0, T, every):
+                        g.sim_run(worker[c:c + every], tau[c:c + every], K)
+                        curve.append(G.gem_diag(g.h).loss / P)
+                table.append({"lr": lr, "n": n, "rule": name, "commits_per_point": every,
+                              "loss_per_param": curve})
+    return {"experiment": "rule comparison on a synthetic quadratic", "P": P, "T": T, "K": K,
+            "sigma": 0.1, "data": "synthetic", "table": table}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +152,9 @@ def main() -> int:
                     help="skip the oracle timing (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the copy kernel (counter calibration) and exit")
+    ap.add_argument("--compare", action="store_true",
+                    help="only run the rule comparison (GEM, DOWNPOUR, adaptive staleness over "
+                         "worker counts and learning rates) and print its loss table")
     ap.add_argument("--cpu-sample-elems", type=int, default=1 << 20)
     ap.add_argument("--cpu-sample-commits", type=int, default=256)
     args = ap.parse_args()
@@ -141,6 +181,10 @@ def main() -> int:
         print(json.dumps({"copy_probe_bytes": 1 << 30, "copy_GBps": gbs}), flush=True)
         return 0
 
+    if args.compare:
+        print(json.dumps(compare_rules(G)), flush=True)
+        return 0
+
     wl = WORKLOADS[args.workload]
     h, ts = problem(wl)
     total = (args.warmup + args.steps) * wl.T
@@ -152,9 +196,8 @@ def main() -> int:
     hp.pi_mode = G.GEM_PI_LITERAL if args.pi == "literal" else G.GEM_PI_CLAMP0
     hp.proxy_mode = G.GEM_PROXY_GLOBAL if args.proxy == "global" else G.GEM_PROXY_LOCAL
     hp.kappa = args.kappa
-    default_rule = (args.rule, args.pi, args.proxy, args.kappa) == ("gem", "clamp0", "local", 1.0)
-    variant = ("General" if (args.rule, args.pi, args.kappa) != ("gem", "clamp0", 1.0)
-               else "FastGlobal" if args.proxy == "global" else "Fast")
+    fast = (args.rule, args.pi, args.kappa) == ("gem", "clamp0", 1.0)
+    variant = "General" if not fast else "FastGlobal" if args.proxy == "global" else "Fast"
 
     stream = torch.cuda.current_stream()
     g = G.Gem(wl.P, wl.n, hp, stream=stream.cuda_stream)
@@ -194,7 +237,7 @@ def main() -> int:
     alg_per_pass = stats.alg_bytes / passes
     avg_pass_s = elapsed / passes
     achieved = alg_per_pass / avg_pass_s / 1e9
-    traffic = measured_traffic(wl.name) if default_rule else None
+    traffic = measured_traffic(wl.name, args.proxy) if fast else None
 
     result = {
         "metric": METRIC,

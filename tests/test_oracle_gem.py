@@ -407,3 +407,48 @@ def test_scale_factors_decrease_with_more_workers():
     for k in range(3):
         assert all(a[k] >= b[k] for a, b in zip(quart, quart[1:]))
     assert quart[0][1] > quart[1][1] > quart[2][1]
+
+
+def _loss_curve(rule, lr, momentum, n, h, ts, T=3000, every=500, seed=9):
+    P = h.size
+    w, tau = O.schedule(n, T, O.LAW_EXP, 0, 0, seed=n)
+    hp = O.Hyper(lr=lr, sigma=0.1, momentum=momentum, rule=rule, seed=seed)
+    st = O.State.initial(n, P)
+    out = []
+    for c in range(0, T, every):
+        O.run(hp, P, st, np.arange(P), h, ts, w[c:c + every], tau[c:c + every])
+        out.append(O.loss(st.theta, h, ts))
+    return np.array(out)
+
+
+def test_gem_stays_stable_as_workers_are_added():
+    """Sec. 4 (stability; update rescaling): GEM keeps to the target dynamics
+    as workers are added.  On the tiny problem (eta = 0.01, mu = 0.9) the loss
+    falls at every checkpoint for n = 1 .. 30, and with 30 workers it stays
+    within 4x of the single worker's loss, while plain stale updates
+    (DOWNPOUR) and the adaptive-staleness rule stay above GEM for every n."""
+    h, ts = _quadratic(2048, 31)
+    finals = {}
+    for n in (1, 5, 10, 20, 30):
+        g = _loss_curve(O.RULE_GEM, 0.01, 0.9, n, h, ts)
+        assert np.all(np.diff(g) < 0), (n, g)
+        finals[n] = g[-1]
+        for rule in (O.RULE_DOWNPOUR, O.RULE_ADAPTIVE):
+            other = _loss_curve(rule, 0.01, 0.0, n, h, ts)
+            assert other[-1] > g[-1], (n, rule, other[-1], g[-1])
+    assert finals[30] < 4 * finals[1]
+
+
+def test_misspecified_learning_rate():
+    """Sec. 4 (misspecified learning rate): with a learning rate the
+    synchronous process still tolerates, stale DOWNPOUR updates diverge once
+    enough workers commit, while GEM stays at the single-worker level.  Tiny
+    problem, eta = 0.5, n = 20, 3000 commits."""
+    h, ts = _quadratic(2048, 31)
+    loss0 = O.loss(np.zeros(2048, dtype=np.float32), h, ts)
+    dp = _loss_curve(O.RULE_DOWNPOUR, 0.5, 0.0, 20, h, ts)
+    gem1 = _loss_curve(O.RULE_GEM, 0.5, 0.9, 1, h, ts)
+    gem20 = _loss_curve(O.RULE_GEM, 0.5, 0.9, 20, h, ts)
+    assert not np.isfinite(dp[-1]) or dp[-1] > 1e6 * loss0, dp
+    assert np.all(np.isfinite(gem20)) and gem20.max() < 0.5 * loss0, gem20
+    assert gem20[-1] < 2 * gem1[-1], (gem20[-1], gem1[-1])
