@@ -98,6 +98,12 @@ def lib():
                                       i64p, C.c_int64, i32p, i32p, C.c_int64, f32p,
                                       C.POINTER(C.c_uint16), C.c_void_p, f32p,
                                       C.POINTER(C.c_uint32)]
+        L.or_sumsq.restype = C.c_double
+        L.or_sumsq.argtypes = [f32p, C.c_int64, C.c_int64]
+        L.or_run_segments.restype = C.c_int
+        L.or_run_segments.argtypes = [C.POINTER(OracleConfig), C.c_int32, i64p, f32p, f32p,
+                                      f32p, f32p, f32p, i64p, C.c_int64, i32p, i32p, C.c_int64,
+                                      f32p, C.POINTER(C.c_uint16), f32p, f32p]
         L.or_pi_bin.restype = C.c_int
         L.or_pi_bin.argtypes = [C.c_float]
         L.or_pi_bin_array.argtypes = [f32p, i32p, C.c_int64]
@@ -313,6 +319,60 @@ def commit_given(hp: Hyper, st: State, worker, d, tau=None, diag: bool = False,
         raise OracleError(rc)
     st.t += K
     return dg, tr
+
+
+def sumsq(x, lo: int = 0, hi: int | None = None) -> float:
+    """Sum of squares of x[lo:hi] in binary64, in the order that defines the
+    segment norms (see or_sumsq): adjacent-pairs tree within aligned groups of
+    1024 indices, then the groups in increasing order."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    hi = x.size if hi is None else hi
+    return float(lib().or_sumsq(_ptr(x, C.c_float), lo, hi))
+
+
+def run_segments(hp: Hyper, st: State, seg_off, worker, tau=None, h=None, ts=None, d=None,
+                 pi: bool = False, trace: bool = False):
+    """Commits with one scale factor per segment [seg_off[k], seg_off[k+1]) of the
+    parameter vector (norms over the segment in eq. 18; see or_run_segments).
+
+    Updates are generated at the snapshots from (h, ts) as in ``run`` (on all P
+    elements) when ``d`` is None, else given as d[T, P] (float32, or uint16
+    bf16 bit patterns).  Returns (pi [T, nseg] or None, trace [T, P, 3] of
+    (a, d, m) or None).
+    """
+    n, P = st.S.shape
+    seg_off = np.ascontiguousarray(seg_off, dtype=np.int64)
+    nseg = seg_off.size - 1
+    worker = np.ascontiguousarray(worker, dtype=np.int32)
+    T = worker.size
+    tau_a = None if tau is None else np.ascontiguousarray(tau, dtype=np.int32)
+    df = db = None
+    if d is not None:
+        d = np.ascontiguousarray(d)
+        assert d.shape == (T, P)
+        if d.dtype == np.float32:
+            df = _ptr(d, C.c_float)
+        elif d.dtype == np.uint16:
+            db = _ptr(d, C.c_uint16)
+        else:
+            raise TypeError("updates must be float32 or uint16 (bfloat16 bits)")
+    else:
+        h = np.ascontiguousarray(h, dtype=np.float32)
+        ts = np.ascontiguousarray(ts, dtype=np.float32)
+        assert h.size == P and ts.size == P
+    po = np.zeros((T, nseg), dtype=np.float32) if pi else None
+    tr = np.zeros((T, P, 3), dtype=np.float32) if trace else None
+    cfg = hp.cfg(P, n)
+    rc = lib().or_run_segments(C.byref(cfg), nseg, _ptr(seg_off, C.c_int64), _ptr(h, C.c_float),
+                               _ptr(ts, C.c_float), _ptr(st.theta, C.c_float),
+                               _ptr(st.S, C.c_float), _ptr(st.M, C.c_float),
+                               _ptr(st.pc, C.c_int64), st.t, _ptr(worker, C.c_int32),
+                               _ptr(tau_a, C.c_int32), T, df, db, _ptr(po, C.c_float),
+                               _ptr(tr, C.c_float))
+    if rc != 0:
+        raise OracleError(rc)
+    st.t += T
+    return po, tr
 
 
 def loss(theta, h, ts) -> float:

@@ -543,6 +543,134 @@ int or_commit_given(const or_config* c, int64_t P, float* theta, float* S, float
     return OR_OK;
 }
 
+/* ------------------------------------------------------------------------- */
+/* Segment-norm scale factors.                                                */
+/*                                                                            */
+/* Eq. (18) divides absolute values element by element.  The same energy      */
+/* argument (eqs. 11-13, triangle inequality) holds with Euclidean norms over */
+/* any block of parameters, which gives one scale factor per segment of the   */
+/* parameter vector (a tensor, or the whole vector for a global norm):       */
+/*   pi_T = (k_eff ||m_T|| - ||theta_T - s_T||) / (||dtheta_T|| + eps),       */
+/* applied as theta_i <- theta_i + pi_T dtheta_i for i in T.  With segments  */
+/* of one element the norms are absolute values and this is eq. (18).        */
+/*                                                                            */
+/* A sum of squares over a segment is a sum of many terms, so its order is   */
+/* part of the definition:                                                    */
+/*   - every term x_i^2 of binary32 x_i is formed exactly in binary64;       */
+/*   - indices are split into aligned groups of 1024 (group g holds          */
+/*     i = 1024 g .. 1024 g + 1023); terms of the group outside the segment  */
+/*     count as zero;                                                         */
+/*   - a group's 1024 terms are added by the adjacent-pairs binary tree:     */
+/*     (0+1), (2+3), ..., then ((0+1)+(2+3)), and so on up to one value;     */
+/*   - the group values are added, in increasing g, to a running total that  */
+/*     starts at zero.                                                        */
+/* The norm is the binary64 square root of that total, rounded to binary32;  */
+/* pi_T then follows the binary32 steps of or_commit_element.                */
+/* ------------------------------------------------------------------------- */
+#define OR_SEG_GROUP 1024
+
+double or_sumsq(const float* x, int64_t lo, int64_t hi)
+{
+    double total = 0.0;
+    double v[OR_SEG_GROUP];
+    if (hi <= lo) return 0.0;
+    for (int64_t g = lo / OR_SEG_GROUP; g * OR_SEG_GROUP < hi; ++g) {
+        for (int k = 0; k < OR_SEG_GROUP; ++k) {
+            const int64_t i = g * OR_SEG_GROUP + k;
+            v[k] = (i >= lo && i < hi) ? (double)x[i] * (double)x[i] : 0.0;
+        }
+        for (int width = 1; width < OR_SEG_GROUP; width *= 2)
+            for (int k = 0; k < OR_SEG_GROUP; k += 2 * width) v[k] = v[k] + v[k + width];
+        total = total + v[0];
+    }
+    return total;
+}
+
+static float or_norm(const float* x, int64_t lo, int64_t hi)
+{
+    return (float)sqrt(or_sumsq(x, lo, hi));
+}
+
+/*
+ * T commits on all P = c->P elements with one scale factor per segment
+ * [seg_off[k], seg_off[k+1]), seg_off[0] = 0 < ... < seg_off[nseg] = P.
+ * Updates are generated at the snapshots as in or_run when d and db are both
+ * NULL, else given as in or_commit_given.  GEM rule only.  pi_out, if given,
+ * receives the applied pi of every segment of every commit (T * nseg);
+ * trace, if given, (a, d, m) of every element of every commit (T * P * 3).
+ */
+int or_run_segments(const or_config* c, int32_t nseg, const int64_t* seg_off,
+                    const float* h, const float* ts, float* theta, float* S, float* M,
+                    int64_t* pc, int64_t t0, const int32_t* worker, const int32_t* tau,
+                    int64_t T, const float* d, const uint16_t* db, float* pi_out, float* trace)
+{
+    if (!c || c->n <= 0 || c->P < 0 || T < 0 || nseg < 1 || !seg_off) return OR_EINVAL;
+    if (c->rule != OR_RULE_GEM) return OR_EINVAL;
+    if (seg_off[0] != 0 || seg_off[nseg] != c->P) return OR_EINVAL;
+    for (int32_t k = 0; k < nseg; ++k)
+        if (seg_off[k + 1] <= seg_off[k]) return OR_EINVAL;
+    if (!d && !db && (!h || !ts)) return OR_EINVAL;
+    int rc = or_check_schedule(c, pc, t0, worker, tau, T);
+    if (rc) return rc;
+    const int64_t P = c->P;
+    float* dv = (float*)malloc(sizeof(float) * (size_t)(P > 0 ? P : 1));
+    float* mv = (float*)malloc(sizeof(float) * (size_t)(P > 0 ? P : 1));
+    float* av = (float*)malloc(sizeof(float) * (size_t)(P > 0 ? P : 1));
+    if (!dv || !mv || !av) { free(dv); free(mv); free(av); return OR_ENOMEM; }
+    const float k_eff = or_k_eff(c);
+    const float neg_lr = -c->lr;
+    for (int64_t j = 0; j < T; ++j) {
+        const int32_t w = worker[j];
+        const int64_t t = t0 + j;
+        const int64_t mrow = (c->proxy == OR_PROXY_GLOBAL) ? 0 : w;
+        float* s_row = &S[(int64_t)w * P];
+        float* m_row = &M[mrow * P];
+        /* The update, the refreshed first moment (Alg. 1, eq. 23) and the
+         * drift theta_t - s_t (eq. 16), element by element. */
+        for (int64_t i = 0; i < P; ++i) {
+            float di;
+            if (d) {
+                di = d[j * P + i];
+            } else if (db) {
+                di = or_bits_to_float((uint32_t)db[j * P + i] << 16);
+            } else {
+                float xi = or_normal(c->seed, (uint32_t)t, i);
+                float g = fmaf(h[i], s_row[i] - ts[i], c->sigma * xi);
+                di = neg_lr * g;
+                if (c->bf16) di = or_round_bf16(di);
+            }
+            dv[i] = di;
+            mv[i] = fmaf(c->momentum, m_row[i], di);
+            av[i] = theta[i] - s_row[i];
+        }
+        if (trace)
+            for (int64_t i = 0; i < P; ++i) {
+                trace[(j * P + i) * 3 + 0] = av[i];
+                trace[(j * P + i) * 3 + 1] = dv[i];
+                trace[(j * P + i) * 3 + 2] = mv[i];
+            }
+        for (int32_t k = 0; k < nseg; ++k) {
+            const int64_t lo = seg_off[k], hi = seg_off[k + 1];
+            /* Eq. (18) with norms over the segment. */
+            float num = k_eff * or_norm(mv, lo, hi) - or_norm(av, lo, hi);
+            float den = or_norm(dv, lo, hi) + c->eps;
+            float pi = num / den;
+            if (c->pi_mode == OR_PI_CLAMP0) pi = (pi > 0.0f) ? pi : 0.0f;
+            if (pi_out) pi_out[j * nseg + k] = pi;
+            for (int64_t i = lo; i < hi; ++i) {
+                const float th_old = theta[i];
+                const float th_new = fmaf(pi, dv[i], th_old);   /* eq. (3) */
+                m_row[i] = mv[i];
+                s_row[i] = (c->pull_mode == OR_PULL_PRE) ? th_old : th_new;
+                theta[i] = th_new;
+            }
+        }
+        pc[w] = (c->pull_mode == OR_PULL_PRE) ? t : t + 1;
+    }
+    free(dv); free(mv); free(av);
+    return OR_OK;
+}
+
 /* Loss of the diagonal quadratic, 1/2 sum h (theta - theta*)^2, in binary64. */
 double or_loss(const float* theta, const float* h, const float* ts, int64_t cnt)
 {
