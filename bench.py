@@ -148,6 +148,8 @@ def main() -> int:
     ap.add_argument("--pi", default="clamp0", choices=["clamp0", "literal"])
     ap.add_argument("--proxy", default="local", choices=["local", "global"])
     ap.add_argument("--kappa", type=float, default=1.0)
+    ap.add_argument("--pi-scope", default="element", choices=["element", "segment"],
+                    help="pi per parameter, or per segment from norms (one global segment)")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle timing (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -196,7 +198,8 @@ def main() -> int:
     hp.pi_mode = G.GEM_PI_LITERAL if args.pi == "literal" else G.GEM_PI_CLAMP0
     hp.proxy_mode = G.GEM_PROXY_GLOBAL if args.proxy == "global" else G.GEM_PROXY_LOCAL
     hp.kappa = args.kappa
-    fast = (args.rule, args.pi, args.kappa) == ("gem", "clamp0", 1.0)
+    hp.pi_scope = G.GEM_PI_SEGMENT if args.pi_scope == "segment" else G.GEM_PI_ELEMENT
+    fast = (args.rule, args.pi, args.kappa, args.pi_scope) == ("gem", "clamp0", 1.0, "element")
     variant = "General" if not fast else "FastGlobal" if args.proxy == "global" else "Fast"
 
     stream = torch.cuda.current_stream()
@@ -261,6 +264,7 @@ def main() -> int:
                            3: "pareto"}[wl.law],
             "passes_per_step": passes / args.steps,
             "rule": args.rule, "pi": args.pi, "proxy": args.proxy, "kappa": args.kappa,
+            "pi_scope": args.pi_scope,
             "parallelism": "single-gpu",
         },
         "roofline": {
@@ -272,7 +276,8 @@ def main() -> int:
             "traffic": traffic,
             "alg_bytes_per_launch": alg_per_pass,
             "avg_launch_ms": avg_pass_s * 1e3,
-            "kernel": "pass_kernel<Generated, %s>" % variant,
+            "kernel": ("seg_step_kernel + seg_reduce_kernel" if args.pi_scope == "segment"
+                       else "pass_kernel<Generated, %s>" % variant),
             "copy_ceiling_GBps": copy_gbs,
             "frac_of_copy": achieved / copy_gbs,
         },

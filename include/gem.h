@@ -58,6 +58,7 @@ enum { GEM_KAPPA_LINEAR = 0, GEM_KAPPA_SQRT = 1 };         /* appendix B forms  
 enum { GEM_PULL_POST_COMMIT = 0, GEM_PULL_PRE_COMMIT = 1 };/* when S[w] is taken  */
 enum { GEM_RULE_GEM = 0, GEM_RULE_DOWNPOUR = 1, GEM_RULE_ADAPTIVE = 2 };
 enum { GEM_PROXY_LOCAL = 0, GEM_PROXY_GLOBAL = 1 };        /* where m lives       */
+enum { GEM_PI_ELEMENT = 0, GEM_PI_SEGMENT = 1 };           /* scope of one pi     */
 enum { GEM_LAW_EXP = 0, GEM_LAW_EXP_UNIFORM_MEAN = 1, GEM_LAW_EXP_LOGNORMAL_MEAN = 2,
        GEM_LAW_PARETO = 3 };
 enum { GEM_SNAPSHOT = 0, GEM_MOMENT = 1 };
@@ -76,7 +77,10 @@ typedef struct gem_handle gem_t;
  * Sec. 4: DOWNPOUR (commit dtheta unchanged, eq. 1) and adaptive staleness
  * (commit dtheta / (tau + 1)).  proxy_mode LOCAL keeps one first moment per
  * worker (Sec. 3.3); GLOBAL keeps one moment shared by all workers, refreshed
- * by every commit (the global proxy of Sec. 6), stored as row 0 of M. */
+ * by every commit (the global proxy of Sec. 6), stored as row 0 of M.
+ * pi_scope ELEMENT computes pi per parameter from absolute values (eq. 18);
+ * SEGMENT computes one pi per segment of the parameter vector from Euclidean
+ * norms over the segment (see gem_set_segments; GEM rule only). */
 typedef struct {
     float momentum;
     float eps;
@@ -86,6 +90,7 @@ typedef struct {
     int32_t pull_mode;
     int32_t rule;
     int32_t proxy_mode;
+    int32_t pi_scope;
 } gem_hyperparams;
 
 /* Stale-gradient generator of the simulated workers: a worker whose snapshot
@@ -138,7 +143,7 @@ const char* gem_strerror(int code);
 const char* gem_last_error(void);
 
 /* Fill hp with Alg. 1's defaults: momentum 0.9, eps 1e-16, kappa 1, CLAMP0,
- * LINEAR, POST_COMMIT, GEM, LOCAL.  Returns GEM_EINVAL if hp is NULL. */
+ * LINEAR, POST_COMMIT, GEM, LOCAL, ELEMENT.  Returns GEM_EINVAL if hp is NULL. */
 int gem_hyperparams_default(gem_hyperparams* hp);
 
 /* Create a master for P parameters and n workers on the current HIP device.
@@ -251,6 +256,32 @@ int gem_diag(gem_t* g, gem_diag_t* out);
  * each -- for at most max_commits commits into out (host), sets *commits to
  * the number recorded, and stops recording.  Errors: EINVAL, ENOMEM, ESTATE
  * (read without a recording). */
+/*
+ * Segments for pi_scope GEM_PI_SEGMENT: count >= 1 segments
+ * [offsets[k], offsets[k+1]) of the parameter vector, offsets a host array of
+ * count + 1 values with offsets[0] = 0 < offsets[1] < ... < offsets[count] = P
+ * (for instance the tensors of a model; one segment [0, P) gives a global
+ * norm, the default).  A commit by worker w then applies, for each segment T
+ * (eqs. 11-13 and 18 with the absolute values replaced by norms over T):
+ *
+ *     m     = mu * M[w] + dtheta                        (every element)
+ *     pi_T  = (kappa_eff ||m_T|| - ||theta_T - S[w]_T||) / (||dtheta_T|| + eps)
+ *     theta = theta + pi_T * dtheta                     (every element of T)
+ *
+ * with pi_mode as for element-wise pi.  A sum of squares is taken in
+ * binary64 in a fixed order (exact squares; aligned blocks of 2^18 indices
+ * added by the adjacent-pairs tree, then the blocks in increasing order), the
+ * norm is its binary64 square root rounded to binary32, and pi_T follows in
+ * binary32; segments of one element give element-wise GEM bit for bit.
+ * Each commit is one streaming launch plus two small reduction launches (a
+ * commit's pi needs every element of its segment first), so commits are not
+ * fused.  Diagnostics and pi histograms are element-wise only: a commit or
+ * run with either enabled returns GEM_EINVAL under this scope.
+ * The offsets are copied; the call may be made at any time between commits.
+ * GEM_EINVAL for a malformed table.
+ */
+int gem_set_segments(gem_t* g, const int64_t* offsets, int32_t count);
+
 #define GEM_PI_BINS 643
 int gem_pi_hist_start(gem_t* g, int64_t capacity);
 int gem_pi_hist_read(gem_t* g, uint32_t* out, int64_t max_commits, int64_t* commits);

@@ -557,32 +557,36 @@ int or_commit_given(const or_config* c, int64_t P, float* theta, float* S, float
 /* A sum of squares over a segment is a sum of many terms, so its order is   */
 /* part of the definition:                                                    */
 /*   - every term x_i^2 of binary32 x_i is formed exactly in binary64;       */
-/*   - indices are split into aligned groups of 1024 (group g holds          */
-/*     i = 1024 g .. 1024 g + 1023); terms of the group outside the segment  */
-/*     count as zero;                                                         */
-/*   - a group's 1024 terms are added by the adjacent-pairs binary tree:     */
-/*     (0+1), (2+3), ..., then ((0+1)+(2+3)), and so on up to one value;     */
-/*   - the group values are added, in increasing g, to a running total that  */
+/*   - indices are split into aligned blocks of 2^18 (block b holds          */
+/*     i = 2^18 b .. 2^18 b + 2^18 - 1); terms outside the segment count as   */
+/*     zero;                                                                  */
+/*   - a block's terms are added by the adjacent-pairs binary tree: (0+1),   */
+/*     (2+3), ..., then ((0+1)+(2+3)), and so on up to one value;             */
+/*   - the block values are added, in increasing b, to a running total that  */
 /*     starts at zero.                                                        */
 /* The norm is the binary64 square root of that total, rounded to binary32;  */
 /* pi_T then follows the binary32 steps of or_commit_element.                */
 /* ------------------------------------------------------------------------- */
-#define OR_SEG_GROUP 1024
+#define OR_SEG_BLOCK (1 << 18)
+
+/* The adjacent-pairs tree over the aligned index range [base, base + len),
+ * len a power of two: the sum of its two halves, each added the same way; one
+ * index gives its term.  A subtree with no index in [lo, hi) is zero, and
+ * adding zero is exact, so such subtrees are not visited. */
+static double or_tree(const float* x, int64_t lo, int64_t hi, int64_t base, int64_t len)
+{
+    if (base >= hi || base + len <= lo) return 0.0;
+    if (len == 1) return (double)x[base] * (double)x[base];
+    const int64_t half = len / 2;
+    return or_tree(x, lo, hi, base, half) + or_tree(x, lo, hi, base + half, half);
+}
 
 double or_sumsq(const float* x, int64_t lo, int64_t hi)
 {
     double total = 0.0;
-    double v[OR_SEG_GROUP];
     if (hi <= lo) return 0.0;
-    for (int64_t g = lo / OR_SEG_GROUP; g * OR_SEG_GROUP < hi; ++g) {
-        for (int k = 0; k < OR_SEG_GROUP; ++k) {
-            const int64_t i = g * OR_SEG_GROUP + k;
-            v[k] = (i >= lo && i < hi) ? (double)x[i] * (double)x[i] : 0.0;
-        }
-        for (int width = 1; width < OR_SEG_GROUP; width *= 2)
-            for (int k = 0; k < OR_SEG_GROUP; k += 2 * width) v[k] = v[k] + v[k + width];
-        total = total + v[0];
-    }
+    for (int64_t b = lo / OR_SEG_BLOCK; b * OR_SEG_BLOCK < hi; ++b)
+        total = total + or_tree(x, lo, hi, b * OR_SEG_BLOCK, OR_SEG_BLOCK);
     return total;
 }
 

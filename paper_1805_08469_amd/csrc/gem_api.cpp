@@ -15,6 +15,7 @@
 #include "gem_internal.hpp"
 
 using gemk::PassArgs;
+using gemk::SegArgs;
 using gemk::Source;
 
 struct gem_handle {
@@ -42,6 +43,20 @@ struct gem_handle {
     int64_t hist_count = 0;        // commits recorded so far (may exceed hist_cap)
     bool hist_on = false;
     gem_stats_t stats{};
+    // Segment-norm scope: the partition (host copy) and its device tables,
+    // built by gem_set_segments or, with one segment, by the first run.
+    std::vector<int64_t> seg_host;   // [nseg + 1] offsets
+    int64_t* seg_off = nullptr;      // [nseg + 1]
+    int64_t* part_off = nullptr;     // [nseg + 1]
+    int32_t* gseg = nullptr;         // [groups]
+    double* part = nullptr;          // [3][npart] group sums of the current commit
+    int32_t* pair_seg = nullptr;     // [nsup] (segment, index block) pairs
+    int32_t* pair_blk = nullptr;
+    int64_t* sup_off = nullptr;      // [nseg + 1] first index-block slot of each segment
+    double* sup = nullptr;           // [3][nsup] index-block sums
+    float* pi_seg = nullptr;         // [nseg]
+    int64_t npart = 0;
+    int64_t nsup = 0;
 };
 
 namespace {
@@ -73,6 +88,8 @@ bool valid_hp(const gem_hyperparams& hp)
     if (hp.rule != GEM_RULE_GEM && hp.rule != GEM_RULE_DOWNPOUR && hp.rule != GEM_RULE_ADAPTIVE)
         return false;
     if (hp.proxy_mode != GEM_PROXY_LOCAL && hp.proxy_mode != GEM_PROXY_GLOBAL) return false;
+    if (hp.pi_scope != GEM_PI_ELEMENT && hp.pi_scope != GEM_PI_SEGMENT) return false;
+    if (hp.pi_scope == GEM_PI_SEGMENT && hp.rule != GEM_RULE_GEM) return false;
     if (!std::isfinite(hp.momentum) || !std::isfinite(hp.eps) || !std::isfinite(hp.kappa))
         return false;
     if (hp.kappa_mode == GEM_KAPPA_SQRT && hp.kappa < 0.0f) return false;
@@ -290,6 +307,168 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+void free_segments(gem_handle* g)
+{
+    (void)hipFree(g->seg_off);
+    (void)hipFree(g->part_off);
+    (void)hipFree(g->gseg);
+    (void)hipFree(g->part);
+    (void)hipFree(g->pair_seg);
+    (void)hipFree(g->pair_blk);
+    (void)hipFree(g->sup_off);
+    (void)hipFree(g->sup);
+    (void)hipFree(g->pi_seg);
+    g->seg_off = g->part_off = g->sup_off = nullptr;
+    g->gseg = g->pair_seg = g->pair_blk = nullptr;
+    g->part = g->sup = nullptr;
+    g->pi_seg = nullptr;
+    g->npart = g->nsup = 0;
+    g->seg_host.clear();
+}
+
+// Build the device tables of a validated partition (replacing any earlier).
+int build_segments(gem_handle* g, const std::vector<int64_t>& off)
+{
+    const int32_t nseg = static_cast<int32_t>(off.size() - 1);
+    const int64_t groups = (g->Pp + gemk::kSegGroup - 1) / gemk::kSegGroup;
+    std::vector<int64_t> part_off(static_cast<size_t>(nseg) + 1, 0);
+    for (int32_t k = 0; k < nseg; ++k)
+        part_off[k + 1] = part_off[k] + (off[k + 1] - 1) / gemk::kSegGroup - off[k] / gemk::kSegGroup + 1;
+    std::vector<int64_t> sup_off(static_cast<size_t>(nseg) + 1, 0);
+    std::vector<int32_t> pair_seg, pair_blk;
+    for (int32_t s = 0; s < nseg; ++s) {
+        const int64_t b_lo = off[s] / gemk::kSegBlock, b_hi = (off[s + 1] - 1) / gemk::kSegBlock;
+        sup_off[s + 1] = sup_off[s] + (b_hi - b_lo + 1);
+        for (int64_t b = b_lo; b <= b_hi; ++b) {
+            pair_seg.push_back(s);
+            pair_blk.push_back(static_cast<int32_t>(b));
+        }
+    }
+    const int64_t nsup = sup_off[nseg];
+    std::vector<int32_t> gseg(static_cast<size_t>(groups));
+    int32_t k = 0;
+    for (int64_t grp = 0; grp < groups; ++grp) {
+        while (off[k + 1] <= grp * gemk::kSegGroup) ++k;   // every group starts below P
+        gseg[grp] = k;
+    }
+    GEM_HIP(hipStreamSynchronize(g->stream));
+    free_segments(g);
+    const int64_t npart = part_off[nseg];
+    bool ok = hipMalloc(&g->seg_off, off.size() * sizeof(int64_t)) == hipSuccess &&
+              hipMalloc(&g->part_off, part_off.size() * sizeof(int64_t)) == hipSuccess &&
+              hipMalloc(&g->gseg, gseg.size() * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&g->part, static_cast<size_t>(3 * npart) * sizeof(double)) == hipSuccess &&
+              hipMalloc(&g->pair_seg, pair_seg.size() * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&g->pair_blk, pair_blk.size() * sizeof(int32_t)) == hipSuccess &&
+              hipMalloc(&g->sup_off, sup_off.size() * sizeof(int64_t)) == hipSuccess &&
+              hipMalloc(&g->sup, static_cast<size_t>(3 * nsup) * sizeof(double)) == hipSuccess &&
+              hipMalloc(&g->pi_seg, static_cast<size_t>(nseg) * sizeof(float)) == hipSuccess;
+    if (!ok) {
+        (void)hipGetLastError();
+        free_segments(g);
+        return GEM_ENOMEM;
+    }
+    g->npart = npart;
+    g->nsup = nsup;
+    const int rc = [&]() -> int {
+        GEM_HIP(hipMemcpyAsync(g->seg_off, off.data(), off.size() * sizeof(int64_t),
+                               hipMemcpyHostToDevice, g->stream));
+        GEM_HIP(hipMemcpyAsync(g->part_off, part_off.data(), part_off.size() * sizeof(int64_t),
+                               hipMemcpyHostToDevice, g->stream));
+        GEM_HIP(hipMemcpyAsync(g->gseg, gseg.data(), gseg.size() * sizeof(int32_t),
+                               hipMemcpyHostToDevice, g->stream));
+        GEM_HIP(hipMemcpyAsync(g->pair_seg, pair_seg.data(), pair_seg.size() * sizeof(int32_t),
+                               hipMemcpyHostToDevice, g->stream));
+        GEM_HIP(hipMemcpyAsync(g->pair_blk, pair_blk.data(), pair_blk.size() * sizeof(int32_t),
+                               hipMemcpyHostToDevice, g->stream));
+        GEM_HIP(hipMemcpyAsync(g->sup_off, sup_off.data(), sup_off.size() * sizeof(int64_t),
+                               hipMemcpyHostToDevice, g->stream));
+        GEM_HIP(hipStreamSynchronize(g->stream));
+        return GEM_OK;
+    }();
+    if (rc != GEM_OK) {
+        free_segments(g);
+        return rc;
+    }
+    g->seg_host = off;
+    return GEM_OK;
+}
+
+// Commits with one scale factor per segment.  Each commit is a step launch
+// (finish the previous commit, start this one), the index-block sums and a
+// per-segment reduction;
+// a last step launch finishes the final commit, so the state in HBM is
+// complete when the call returns to the stream.
+int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
+                 const void* const* upd, bool bf16_out)
+{
+    if (T == 0) return GEM_OK;
+    if (g->seg_host.empty()) {
+        const int rc = build_segments(g, {0, g->P});
+        if (rc) return rc;
+    }
+    const int32_t nseg = static_cast<int32_t>(g->seg_host.size() - 1);
+    SegArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.theta = g->theta;
+    a.S = g->S;
+    a.M = g->M;
+    a.h = g->h;
+    a.ts = g->ts;
+    a.pi_seg = g->pi_seg;
+    a.part = g->part;
+    a.seg_off = g->seg_off;
+    a.part_off = g->part_off;
+    a.gseg = g->gseg;
+    a.npart = g->npart;
+    a.Pp = g->Pp;
+    a.P = g->P;
+    a.pre_pull = g->hp.pull_mode == GEM_PULL_PRE_COMMIT;
+    a.key0 = static_cast<uint32_t>(g->sp.seed);
+    a.key1 = static_cast<uint32_t>(g->sp.seed >> 32);
+    a.neg_lr = -g->sp.lr;
+    a.sigma = g->sp.sigma;
+    a.mu = g->hp.momentum;
+    const float k_eff = kappa_eff(g->hp);
+    const bool literal = g->hp.pi_mode == GEM_PI_LITERAL;
+    // Bytes per element-commit the launches move: theta read and written, the
+    // committing worker's snapshot read and its pull written, the moment read
+    // and written; generated updates read h and theta* and the pending
+    // commit's snapshot (to generate its update again), given updates read
+    // the caller's update twice.
+    const double per_elem = src == Source::Generated ? 36.0 : src == Source::GivenF32 ? 32.0 : 28.0;
+    for (int64_t j = 0; j < T; ++j) {
+        const int32_t w = worker[j];
+        const int64_t t = g->t;
+        a.apply = j > 0;
+        a.start = 1;
+        a.w_prev = j > 0 ? worker[j - 1] : 0;
+        a.w_cur = w;
+        a.m_row = g->hp.proxy_mode == GEM_PROXY_GLOBAL ? 0 : w;
+        a.t = static_cast<uint32_t>(t);
+        a.upd_prev = (upd && j > 0) ? upd[j - 1] : nullptr;
+        a.upd_cur = upd ? upd[j] : nullptr;
+        GEM_HIP(gemk::launch_seg_step(a, src, bf16_out, g->stream));
+        GEM_HIP(gemk::launch_seg_blocks(g->part, g->npart, g->part_off, g->seg_off, g->pair_seg,
+                                        g->pair_blk, g->nsup, g->sup, g->sup_off, g->stream));
+        GEM_HIP(gemk::launch_seg_reduce(g->sup, g->nsup, g->sup_off, nseg, g->pi_seg, k_eff,
+                                        g->hp.eps, literal, g->stream));
+        g->pc[w] = next_pull(g, t);
+        g->t += 1;
+        g->stats.commits += 1;
+        g->stats.passes += 1;
+        g->stats.alg_bytes += per_elem * static_cast<double>(g->Pp);
+    }
+    a.apply = 1;
+    a.start = 0;
+    a.t = static_cast<uint32_t>(g->t);
+    a.w_prev = worker[T - 1];
+    a.upd_prev = upd ? upd[T - 1] : nullptr;
+    a.upd_cur = nullptr;
+    GEM_HIP(gemk::launch_seg_step(a, src, bf16_out, g->stream));
+    return GEM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -325,6 +504,7 @@ int gem_hyperparams_default(gem_hyperparams* hp)
     hp->pull_mode = GEM_PULL_POST_COMMIT;
     hp->rule = GEM_RULE_GEM;
     hp->proxy_mode = GEM_PROXY_LOCAL;
+    hp->pi_scope = GEM_PI_ELEMENT;
     return GEM_OK;
 }
 
@@ -340,6 +520,7 @@ int gem_destroy(gem_t* g)
     (void)hipFree(g->acc);
     (void)hipFree(g->sink);
     (void)hipFree(g->pi_hist);
+    free_segments(g);
     delete g;
     return GEM_OK;
 }
@@ -458,10 +639,23 @@ int gem_commit_batch(gem_t* g, int32_t K, const void* const* dthetas_dev, int32_
     }
     int rc = check_sequence(g, worker_ids, staleness, K);
     if (rc) return rc;
+    const Source src = dtype == GEM_F32 ? Source::GivenF32 : Source::GivenBF16;
+    if (g->hp.pi_scope == GEM_PI_SEGMENT) {
+        if (g->diag_on || g->hist_on) return GEM_EINVAL;
+        return run_segments(g, worker_ids, K, src, dthetas_dev, false);
+    }
     std::vector<Pass> passes;
     plan_passes(g, worker_ids, K, GEM_K_MAX, passes);
-    return run_passes(g, passes, dtype == GEM_F32 ? Source::GivenF32 : Source::GivenBF16,
-                      dthetas_dev, false);
+    return run_passes(g, passes, src, dthetas_dev, false);
+}
+
+int gem_set_segments(gem_t* g, const int64_t* offsets, int32_t count)
+{
+    if (!g || !offsets || count < 1) return GEM_EINVAL;
+    if (offsets[0] != 0 || offsets[count] != g->P) return GEM_EINVAL;
+    for (int32_t k = 0; k < count; ++k)
+        if (offsets[k + 1] <= offsets[k]) return GEM_EINVAL;
+    return build_segments(g, std::vector<int64_t>(offsets, offsets + count + 1));
 }
 
 int gem_commit(gem_t* g, const float* dtheta_dev, int32_t worker_id)
@@ -492,6 +686,11 @@ int gem_sim_run(gem_t* g, const int32_t* worker, const int32_t* tau, int64_t T, 
     if (!g->have_problem) return GEM_ESTATE;
     int rc = check_sequence(g, worker, tau, T);
     if (rc) return rc;
+    if (g->hp.pi_scope == GEM_PI_SEGMENT) {
+        if (g->diag_on || g->hist_on) return GEM_EINVAL;
+        return run_segments(g, worker, T, Source::Generated, nullptr,
+                            g->sp.update_dtype == GEM_BF16);
+    }
     std::vector<Pass> passes;
     plan_passes(g, worker, T, K, passes);
     return run_passes(g, passes, Source::Generated, nullptr, g->sp.update_dtype == GEM_BF16);

@@ -75,6 +75,44 @@ struct PassArgs {
 
 enum class Source { Generated = 0, GivenF32 = 1, GivenBF16 = 2 };
 
+// Segment-norm scale factors.  A sum of squares is the adjacent-pairs tree
+// over aligned blocks of kSegBlock indices, then the blocks in order.  The
+// step kernel forms the tree's lower levels, one aligned group of
+// kSegGroup = 4 * 256 indices per thread block; seg_blocks_kernel the upper
+// levels, 256 groups per index block.
+constexpr int64_t kSegGroup = 1024;
+constexpr int64_t kSegBlock = 1 << 18;
+
+// One launch of the segment step kernel: finish the pending commit (apply its
+// per-segment factors and pull) and/or start commit t (form d, m and the
+// drift, store m, and write the group sums of squares of the drift, m and d
+// for every segment the group touches).
+struct SegArgs {
+    float* theta;             // [Pp]
+    float* S;                 // [n][Pp]
+    float* M;                 // [n][Pp]
+    const float* h;           // [Pp]   (generated updates)
+    const float* ts;          // [Pp]
+    const void* upd_prev;     // caller update of the pending commit (given updates)
+    const void* upd_cur;      // caller update of commit t (given updates)
+    const float* pi_seg;      // [nseg] factors of the pending commit
+    double* part;             // [3][npart] group sums of squares of commit t: drift, m, d
+    const int64_t* seg_off;   // [nseg + 1]
+    const int64_t* part_off;  // [nseg + 1] first group-sum slot of each segment
+    const int32_t* gseg;      // [groups] segment holding each group's first element
+    int64_t npart;
+    int64_t Pp, P;
+    int32_t apply;            // finish the pending commit
+    int32_t start;            // start commit t
+    int32_t w_prev;           // worker of the pending commit
+    int32_t w_cur;            // worker of commit t
+    int32_t m_row;            // row of M that commit t refreshes
+    int32_t pre_pull;         // the snapshot keeps the pre-commit theta
+    uint32_t t;               // clock of commit t; the pending commit's is t - 1
+    uint32_t key0, key1;
+    float neg_lr, sigma, mu;
+};
+
 // Pass-kernel specialisations.  Fast and FastGlobal take the default rule
 // (GEM, CLAMP0, kappa_eff = 1, post-commit pull) with per-worker or shared
 // first moments; General takes every mode as uniform runtime flags.
@@ -83,6 +121,14 @@ enum class Variant { General = 0, Fast = 1, FastGlobal = 2 };
 // Launchers (defined in gem_kernels.hip).
 hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
                        hipStream_t stream);
+hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream);
+hipError_t launch_seg_blocks(const double* part, int64_t npart, const int64_t* part_off,
+                             const int64_t* seg_off, const int32_t* pair_seg,
+                             const int32_t* pair_blk, int64_t npairs, double* sup,
+                             const int64_t* sup_off, hipStream_t stream);
+hipError_t launch_seg_reduce(const double* sup, int64_t nsup, const int64_t* sup_off,
+                             int32_t nseg, float* pi_seg, float k_eff, float eps, bool literal,
+                             hipStream_t stream);
 hipError_t launch_generate(const float* S_w, const float* h, const float* ts, void* out,
                            bool bf16, int64_t P, uint32_t t, uint32_t key0, uint32_t key1,
                            float neg_lr, float sigma, hipStream_t stream);

@@ -375,6 +375,249 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     }
 }
 
+// ---------------------------------------------------------------------------
+// Segment-norm scale factors (one pi per segment of the parameter vector).
+// A commit's pi needs sums of squares over whole segments, so each commit is
+// split in two launches: the step kernel starts commit t (forms d, m and the
+// drift, stores m and d, writes group sums of squares) and the reduction
+// turns the group sums into one pi per segment; the next step kernel applies
+// those factors (and the pull) before starting the next commit.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float4 f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+// c ? x : y on values (a conditional on two float4 objects selects between
+// their addresses, which keeps them out of registers).
+__device__ __forceinline__ float4 pick(bool c, float4 x, float4 y)
+{
+    return make_float4(c ? x.x : y.x, c ? x.y : y.y, c ? x.z : y.z, c ? x.w : y.w);
+}
+__device__ __forceinline__ float lane(const float4& v, int k)
+{
+    return k == 0 ? v.x : k == 1 ? v.y : k == 2 ? v.z : v.w;
+}
+
+// Sum of the block's 256 per-thread values by the adjacent-pairs tree: lane
+// butterflies (which add pairs 2k, 2k+1, then pairs of pairs, ...) within
+// each wave, then (wave 0 + wave 1) + (wave 2 + wave 3).  Thread 0 gets the
+// result.  Every thread of the block must call it.
+__device__ __forceinline__ double block_tree_sum(double v, double* lds)
+{
+#pragma unroll
+    for (int mask = 1; mask < 64; mask <<= 1) v = v + __shfl_xor(v, mask);
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) lds[wave] = v;
+    __syncthreads();
+    const double r = (lds[0] + lds[1]) + (lds[2] + lds[3]);
+    __syncthreads();
+    return r;
+}
+
+template <Source SRC, bool BF16>
+__global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
+{
+    static_assert(kBlock * 4 == kSegGroup, "one block per group of sums");
+    __shared__ double lds[3][4];
+    const int64_t grp = blockIdx.x;
+    const int64_t c = grp * kBlock + threadIdx.x;
+    const bool active = c < (a.Pp >> 2);   // the last group may hold fewer chunks
+    const int64_t off = c * 4;
+    const int32_t s_first = a.gseg[grp];
+
+    float4 th = active ? f4(a.theta + off) : make_float4(0.f, 0.f, 0.f, 0.f);
+    const float4 th_old = th;
+    float4 hv = make_float4(0.f, 0.f, 0.f, 0.f), tv = hv;
+    if (SRC == Source::Generated && active) {
+        hv = f4(a.h + off);
+        tv = f4(a.ts + off);
+    }
+    if (a.apply && active) {
+        // The pending commit's update: the caller's, or generated again at
+        // the worker's snapshot, which its pull below replaces.
+        float4 d;
+        float* srow = a.S + static_cast<int64_t>(a.w_prev) * a.Pp + off;
+        if (SRC == Source::Generated) {
+            const float4 sp = f4(srow);
+            const float4 z = normals4(static_cast<uint64_t>(c), a.t - 1u, a.key0, a.key1);
+            d.x = stale_update<BF16>(a.neg_lr, a.sigma, sp.x, hv.x, tv.x, z.x);
+            d.y = stale_update<BF16>(a.neg_lr, a.sigma, sp.y, hv.y, tv.y, z.y);
+            d.z = stale_update<BF16>(a.neg_lr, a.sigma, sp.z, hv.z, tv.z, z.z);
+            d.w = stale_update<BF16>(a.neg_lr, a.sigma, sp.w, hv.w, tv.w, z.w);
+        } else {
+            d = load_given<SRC>(a.upd_prev, c, a.P);
+        }
+        // eq. 3 with the factor of each element's segment (padding stays put)
+        int32_t seg = s_first;
+        auto factor = [&](int64_t i) {
+            while (a.seg_off[seg + 1] <= i) ++seg;
+            return a.pi_seg[seg];
+        };
+        if (off + 0 < a.P) th.x = __builtin_fmaf(factor(off + 0), d.x, th.x);
+        if (off + 1 < a.P) th.y = __builtin_fmaf(factor(off + 1), d.y, th.y);
+        if (off + 2 < a.P) th.z = __builtin_fmaf(factor(off + 2), d.z, th.z);
+        if (off + 3 < a.P) th.w = __builtin_fmaf(factor(off + 3), d.w, th.w);
+        *reinterpret_cast<float4*>(srow) = pick(a.pre_pull, th_old, th);
+    }
+    if (!a.start) {
+        if (active) *reinterpret_cast<float4*>(a.theta + off) = th;
+        return;
+    }
+
+    float4 s, d, mo;
+    mo = make_float4(0.f, 0.f, 0.f, 0.f);
+    s = mo;
+    d = mo;
+    if (active) {
+        if (a.apply && a.w_cur == a.w_prev) s = pick(a.pre_pull, th_old, th);   // just pulled
+        else s = f4(a.S + static_cast<int64_t>(a.w_cur) * a.Pp + off);
+        if (SRC == Source::Generated) {
+            const float4 z = normals4(static_cast<uint64_t>(c), a.t, a.key0, a.key1);
+            d.x = stale_update<BF16>(a.neg_lr, a.sigma, s.x, hv.x, tv.x, z.x);
+            d.y = stale_update<BF16>(a.neg_lr, a.sigma, s.y, hv.y, tv.y, z.y);
+            d.z = stale_update<BF16>(a.neg_lr, a.sigma, s.z, hv.z, tv.z, z.z);
+            d.w = stale_update<BF16>(a.neg_lr, a.sigma, s.w, hv.w, tv.w, z.w);
+        } else {
+            d = load_given<SRC>(a.upd_cur, c, a.P);
+        }
+        float* mrow = a.M + static_cast<int64_t>(a.m_row) * a.Pp + off;
+        mo = f4(mrow);
+        float4 m;
+        m.x = __builtin_fmaf(a.mu, mo.x, d.x);     // Alg. 1: m <- mu m + dtheta
+        m.y = __builtin_fmaf(a.mu, mo.y, d.y);
+        m.z = __builtin_fmaf(a.mu, mo.z, d.z);
+        m.w = __builtin_fmaf(a.mu, mo.w, d.w);
+        *reinterpret_cast<float4*>(mrow) = m;
+        *reinterpret_cast<float4*>(a.theta + off) = th;
+        mo = m;
+    }
+    // Terms of the sums of squares: drift theta_t - s_t (eq. 16), m and d.
+    double ta[4], tm[4], td[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const double dr = static_cast<double>(lane(th, k) - lane(s, k));
+        const double mk = static_cast<double>(lane(mo, k));
+        const double dk = static_cast<double>(lane(d, k));
+        ta[k] = dr * dr;
+        tm[k] = mk * mk;
+        td[k] = dk * dk;
+    }
+    // One set of group sums per segment the group touches (terms outside the
+    // segment count as zero); the loop is uniform across the block.
+    const int64_t g_lo = grp * kSegGroup;
+    const int64_t g_hi = (g_lo + kSegGroup < a.P) ? g_lo + kSegGroup : a.P;
+    for (int32_t seg = s_first; a.seg_off[seg] < g_hi; ++seg) {
+        const int64_t lo = a.seg_off[seg], hi = a.seg_off[seg + 1];
+        double ca = 0.0, cm = 0.0, cd = 0.0;
+        if (active) {
+            double xa[4], xm[4], xd[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const bool in = off + k >= lo && off + k < hi;
+                xa[k] = in ? ta[k] : 0.0;
+                xm[k] = in ? tm[k] : 0.0;
+                xd[k] = in ? td[k] : 0.0;
+            }
+            ca = (xa[0] + xa[1]) + (xa[2] + xa[3]);
+            cm = (xm[0] + xm[1]) + (xm[2] + xm[3]);
+            cd = (xd[0] + xd[1]) + (xd[2] + xd[3]);
+        }
+        const double sa = block_tree_sum(ca, lds[0]);
+        const double sm = block_tree_sum(cm, lds[1]);
+        const double sd = block_tree_sum(cd, lds[2]);
+        if (threadIdx.x == 0) {
+            const int64_t q = a.part_off[seg] + (grp - (lo / kSegGroup));
+            a.part[q] = sa;
+            a.part[a.npart + q] = sm;
+            a.part[2 * a.npart + q] = sd;
+        }
+    }
+}
+
+// The tree's upper levels: one block per (segment, aligned block of
+// kSegBlock indices) pair adds the 256 group sums of that index block -- zero
+// for groups outside the segment -- by the same adjacent-pairs tree.
+__global__ __launch_bounds__(kBlock) void seg_blocks_kernel(const double* __restrict__ part,
+                                                            int64_t npart,
+                                                            const int64_t* __restrict__ part_off,
+                                                            const int64_t* __restrict__ seg_off,
+                                                            const int32_t* __restrict__ pair_seg,
+                                                            const int32_t* __restrict__ pair_blk,
+                                                            double* __restrict__ sup, int64_t nsup,
+                                                            const int64_t* __restrict__ sup_off)
+{
+    static_assert(kBlock * kSegGroup == kSegBlock, "one thread per group of an index block");
+    __shared__ double lds[3][4];
+    const int32_t seg = pair_seg[blockIdx.x];
+    const int64_t blk = pair_blk[blockIdx.x];
+    const int64_t g_lo = seg_off[seg] / kSegGroup;
+    const int64_t g_hi = (seg_off[seg + 1] - 1) / kSegGroup;
+    const int64_t grp = blk * kBlock + threadIdx.x;
+    double va = 0.0, vm = 0.0, vd = 0.0;
+    if (grp >= g_lo && grp <= g_hi) {
+        const int64_t q = part_off[seg] + (grp - g_lo);
+        va = part[q];
+        vm = part[npart + q];
+        vd = part[2 * npart + q];
+    }
+    const double sa = block_tree_sum(va, lds[0]);
+    const double sm = block_tree_sum(vm, lds[1]);
+    const double sd = block_tree_sum(vd, lds[2]);
+    if (threadIdx.x == 0) {
+        const int64_t q = sup_off[seg] + (blk - seg_off[seg] / kSegBlock);
+        sup[q] = sa;
+        sup[nsup + q] = sm;
+        sup[2 * nsup + q] = sd;
+    }
+}
+
+// Lane k's binary64 value, read by every lane (the two halves through the
+// scalar unit).
+__device__ __forceinline__ double read_lane(double v, int k)
+{
+    const uint64_t b = static_cast<uint64_t>(__double_as_longlong(v));
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(b)), k);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(b >> 32)), k);
+    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+
+// One wave per segment: add the segment's index-block sums in increasing
+// order (the lanes load 64 at a time; the additions stay in order, on values
+// read lane by lane), take the norms (binary64 square root, rounded to
+// binary32) and form pi as in the element step (eq. 18 with norms).
+__global__ __launch_bounds__(64) void seg_reduce_kernel(const double* __restrict__ sup,
+                                                        int64_t nsup,
+                                                        const int64_t* __restrict__ sup_off,
+                                                        float* __restrict__ pi_seg,
+                                                        float k_eff, float eps, int32_t literal)
+{
+    const int32_t seg = blockIdx.x;
+    const int64_t q0 = sup_off[seg], q1 = sup_off[seg + 1];
+    double sa = 0.0, sm = 0.0, sd = 0.0;
+    for (int64_t base = q0; base < q1; base += 64) {
+        const int64_t q = base + threadIdx.x;
+        double va = 0.0, vm = 0.0, vd = 0.0;
+        if (q < q1) {
+            va = sup[q];
+            vm = sup[nsup + q];
+            vd = sup[2 * nsup + q];
+        }
+        const int cnt = (q1 - base < 64) ? static_cast<int>(q1 - base) : 64;
+        for (int k = 0; k < cnt; ++k) {
+            sa = sa + read_lane(va, k);
+            sm = sm + read_lane(vm, k);
+            sd = sd + read_lane(vd, k);
+        }
+    }
+    if (threadIdx.x != 0) return;
+    const float na = static_cast<float>(sqrt(sa));
+    const float nm = static_cast<float>(sqrt(sm));
+    const float nd = static_cast<float>(sqrt(sd));
+    const float num = k_eff * nm - na;
+    const float den = nd + eps;
+    float pi = num / den;
+    if (!literal) pi = (pi > 0.0f) ? pi : 0.0f;
+    pi_seg[seg] = pi;
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(kBlock) void generate_kernel(const float* __restrict__ S_w,
                                                          const float* __restrict__ h,
@@ -510,6 +753,51 @@ hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, 
         return launch_fd<Source::GivenBF16, false>(a, v, diag, stream);
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream)
+{
+    const unsigned grid = blocks_for(a.Pp >> 2);
+    switch (src) {
+    case Source::Generated:
+        if (bf16_out)
+            hipLaunchKernelGGL((seg_step_kernel<Source::Generated, true>), dim3(grid), dim3(kBlock),
+                               0, stream, a);
+        else
+            hipLaunchKernelGGL((seg_step_kernel<Source::Generated, false>), dim3(grid), dim3(kBlock),
+                               0, stream, a);
+        break;
+    case Source::GivenF32:
+        hipLaunchKernelGGL((seg_step_kernel<Source::GivenF32, false>), dim3(grid), dim3(kBlock), 0,
+                           stream, a);
+        break;
+    case Source::GivenBF16:
+        hipLaunchKernelGGL((seg_step_kernel<Source::GivenBF16, false>), dim3(grid), dim3(kBlock), 0,
+                           stream, a);
+        break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_seg_blocks(const double* part, int64_t npart, const int64_t* part_off,
+                             const int64_t* seg_off, const int32_t* pair_seg,
+                             const int32_t* pair_blk, int64_t npairs, double* sup,
+                             const int64_t* sup_off, hipStream_t stream)
+{
+    if (npairs <= 0) return hipSuccess;
+    hipLaunchKernelGGL(seg_blocks_kernel, dim3(static_cast<unsigned>(npairs)), dim3(kBlock), 0,
+                       stream, part, npart, part_off, seg_off, pair_seg, pair_blk, sup, npairs,
+                       sup_off);
+    return hipGetLastError();
+}
+
+hipError_t launch_seg_reduce(const double* sup, int64_t nsup, const int64_t* sup_off,
+                             int32_t nseg, float* pi_seg, float k_eff, float eps, bool literal,
+                             hipStream_t stream)
+{
+    hipLaunchKernelGGL(seg_reduce_kernel, dim3(static_cast<unsigned>(nseg)), dim3(64), 0, stream,
+                       sup, nsup, sup_off, pi_seg, k_eff, eps, literal ? 1 : 0);
+    return hipGetLastError();
 }
 
 hipError_t launch_generate(const float* S_w, const float* h, const float* ts, void* out, bool bf16,

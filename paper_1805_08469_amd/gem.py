@@ -25,6 +25,7 @@ GEM_KAPPA_LINEAR, GEM_KAPPA_SQRT = 0, 1
 GEM_PULL_POST_COMMIT, GEM_PULL_PRE_COMMIT = 0, 1
 GEM_RULE_GEM, GEM_RULE_DOWNPOUR, GEM_RULE_ADAPTIVE = 0, 1, 2
 GEM_PROXY_LOCAL, GEM_PROXY_GLOBAL = 0, 1
+GEM_PI_ELEMENT, GEM_PI_SEGMENT = 0, 1
 GEM_LAW_EXP, GEM_LAW_EXP_UNIFORM_MEAN, GEM_LAW_EXP_LOGNORMAL_MEAN, GEM_LAW_PARETO = 0, 1, 2, 3
 GEM_SNAPSHOT, GEM_MOMENT = 0, 1
 GEM_K_MAX = 32
@@ -37,14 +38,14 @@ EXPORTED = (
     "gem_sim_run", "gem_read_theta", "gem_read_state", "gem_gather", "gem_clock",
     "gem_pull_clocks", "gem_reset_worker", "gem_diag_enable", "gem_diag_reset", "gem_diag",
     "gem_stats", "gem_stats_reset", "gem_save", "gem_load", "gem_sync", "gem_copy_f32",
-    "gem_pi_hist_start", "gem_pi_hist_read",
+    "gem_pi_hist_start", "gem_pi_hist_read", "gem_set_segments",
 )
 
 
 class gem_hyperparams(C.Structure):
     _fields_ = [("momentum", C.c_float), ("eps", C.c_float), ("kappa", C.c_float),
                 ("pi_mode", C.c_int32), ("kappa_mode", C.c_int32), ("pull_mode", C.c_int32),
-                ("rule", C.c_int32), ("proxy_mode", C.c_int32)]
+                ("rule", C.c_int32), ("proxy_mode", C.c_int32), ("pi_scope", C.c_int32)]
 
 
 class gem_sim_params(C.Structure):
@@ -118,6 +119,7 @@ def _load():
         "gem_sync": (C.c_int, [vp]),
         "gem_copy_f32": (C.c_int, [vp, vp, C.c_int64, vp]),
         "gem_pi_hist_start": (C.c_int, [vp, C.c_int64]),
+        "gem_set_segments": (C.c_int, [vp, i64p, C.c_int32]),
         "gem_pi_hist_read": (C.c_int, [vp, C.POINTER(C.c_uint32), C.c_int64, i64p]),
     }
     for name, (res, args) in sig.items():
@@ -289,6 +291,12 @@ def gem_load(g: int, path: str) -> int:
     return _L.gem_load(g, path.encode())
 
 
+def gem_set_segments(g: int, offsets) -> None:
+    """Segments [offsets[k], offsets[k+1]) for the segment-norm scale factors."""
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    _check(_L.gem_set_segments(g, _p(off, C.c_int64), off.size - 1), "gem_set_segments")
+
+
 def gem_pi_hist_start(g: int, capacity: int) -> None:
     _check(_L.gem_pi_hist_start(g, capacity), "gem_pi_hist_start")
 
@@ -337,6 +345,9 @@ class Gem:
         sp = gem_sim_params(lr=lr, sigma=sigma, seed=seed,
                             update_dtype=GEM_BF16 if bf16 else GEM_F32)
         gem_set_quadratic(self.h, h, ts, sp)
+
+    def set_segments(self, offsets):
+        gem_set_segments(self.h, offsets)
 
     def sim_run(self, worker, tau, K):
         _check(gem_sim_run(self.h, worker, tau, K), "gem_sim_run")

@@ -6,7 +6,8 @@ over segments of the parameter vector: per tensor, or one global norm).
   and given updates.
 * The sum of squares that defines a norm: exact where every partial sum is
   exact (integer-valued terms), and within its error bound of an exactly
-  rounded sum (math.fsum) otherwise, over ragged segment bounds.
+  rounded sum (math.fsum) otherwise, over ragged segment bounds and across
+  the aligned 2^18-index blocks of its tree.
 * One worker, no staleness: a single global segment with mu = 0 is plain SGD
   bit for bit; with momentum the committed update has exactly the proxy's norm
   (the compliance of eq. 13, in norm).
@@ -69,25 +70,26 @@ def test_unit_segments_equal_elementwise_given(dtype):
 
 
 @pytest.mark.parametrize("lo,hi", [(0, 1), (0, 1024), (3, 1025), (1000, 5000), (2047, 2049),
-                                   (0, 9000), (5, 5)])
+                                   (0, 9000), (5, 5), (262_000, 262_200), (1, 600_000)])
 def test_sumsq_exact_on_integer_terms(lo, hi):
     """Integer terms below 2^10 keep every partial sum an integer below 2^53, so
     any order gives the exact sum: a dropped, repeated or misplaced term fails."""
     rng = np.random.default_rng(lo * 7 + hi)
-    x = rng.integers(-1000, 1000, size=9000).astype(np.float32)
+    x = rng.integers(-1000, 1000, size=600_000).astype(np.float32)
     exact = sum(int(v) * int(v) for v in x[lo:hi])
     assert O.sumsq(x, lo, hi) == float(exact)
 
 
-@pytest.mark.parametrize("size,seed", [(1, 0), (1023, 1), (1025, 2), (50_000, 3), (123_457, 4)])
+@pytest.mark.parametrize("size,seed", [(1, 0), (1023, 1), (1025, 2), (50_000, 3),
+                                       (600_001, 4)])
 def test_sumsq_within_error_bound(size, seed):
-    """Against the exactly rounded sum: each of the (log2 1024 + groups) levels
+    """Against the exactly rounded sum: each of the (log2 2^18 + blocks) levels
     of additions contributes at most one rounding of relative 2^-53."""
     rng = np.random.default_rng(seed)
     x = (rng.standard_normal(size) * np.exp(rng.uniform(-20, 20, size))).astype(np.float32)
     lo, hi = size // 7, size
     ref = math.fsum(float(v) * float(v) for v in x[lo:hi])
-    levels = 10 + (hi - 1) // 1024 - lo // 1024 + 1
+    levels = 18 + (hi - 1) // 2 ** 18 - lo // 2 ** 18 + 1
     got = O.sumsq(x, lo, hi)
     assert abs(got - ref) <= levels * 2.0 ** -53 * ref
 
