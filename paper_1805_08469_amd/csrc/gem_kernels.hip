@@ -145,12 +145,6 @@ struct Rows {
     float4 s, m;
 };
 
-__device__ __forceinline__ Rows load_rows(const PassArgs& a, int w, int64_t off)
-{
-    const int64_t row = static_cast<int64_t>(w) * a.Pp + off;
-    return Rows{*reinterpret_cast<const float4*>(a.S + row), *reinterpret_cast<const float4*>(a.M + row)};
-}
-
 
 // Per-thread context of a fused pass: the chunk, its central values and the
 // problem coefficients, kept in registers for the whole pass.

@@ -40,9 +40,9 @@ def test_library_exports_every_declared_symbol():
 def test_defaults_are_alg1():
     hp = G.gem_hyperparams_default()
     assert hp.momentum == pytest.approx(0.9) and hp.eps == np.float32(1e-16) and hp.kappa == 1.0
-    assert (hp.pi_mode, hp.kappa_mode, hp.pull_mode, hp.rule, hp.proxy_mode) == (
+    assert (hp.pi_mode, hp.kappa_mode, hp.pull_mode, hp.rule, hp.proxy_mode, hp.pi_scope) == (
         G.GEM_PI_CLAMP0, G.GEM_KAPPA_LINEAR, G.GEM_PULL_POST_COMMIT, G.GEM_RULE_GEM,
-        G.GEM_PROXY_LOCAL)
+        G.GEM_PROXY_LOCAL, G.GEM_PI_ELEMENT)
 
 
 def test_strerror_covers_codes():
@@ -88,6 +88,13 @@ def test_create_rejects_bad_arguments_before_device_work():
     assert L.gem_create(16, 4, C.byref(hp), None, C.byref(out)) == G.GEM_EINVAL
     hp = G.gem_hyperparams_default()
     hp.proxy_mode = 2
+    assert L.gem_create(16, 4, C.byref(hp), None, C.byref(out)) == G.GEM_EINVAL
+    hp = G.gem_hyperparams_default()
+    hp.pi_scope = 2
+    assert L.gem_create(16, 4, C.byref(hp), None, C.byref(out)) == G.GEM_EINVAL
+    hp = G.gem_hyperparams_default()
+    hp.pi_scope = G.GEM_PI_SEGMENT
+    hp.rule = G.GEM_RULE_ADAPTIVE        # per-segment pi is a GEM-rule scope
     assert L.gem_create(16, 4, C.byref(hp), None, C.byref(out)) == G.GEM_EINVAL
     hp = G.gem_hyperparams_default()
     hp.kappa_mode = G.GEM_KAPPA_SQRT
