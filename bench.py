@@ -232,7 +232,7 @@ def main() -> int:
     stats = G.gem_stats(g.h)
     assert stats.commits == args.steps * wl.T
     g.close()
-    copy_gbs = copy_ceiling(G, torch, 1 << 30)
+    copy_gbs = copy_ceiling(G, torch, 2 << 30)
 
     elapsed = max(gpu_s, 1e-12)
     value = wl.P * stats.commits / elapsed

@@ -692,14 +692,33 @@ __global__ __launch_bounds__(kBlock) void loss_kernel(const float* __restrict__ 
     if (threadIdx.x == 0) atomicAdd(out, red[0]);
 }
 
+// Plain copy, the bandwidth reference: each block moves tiles of
+// kCopyUnroll * kBlock 16-byte chunks, all loads of a tile before its stores.
+constexpr int kCopyUnroll = 4;
+
 __global__ __launch_bounds__(kBlock) void copy_kernel(const float* __restrict__ src,
                                                       float* __restrict__ dst, int64_t count)
 {
     const int64_t n4 = count / 4;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    const float4* s4 = reinterpret_cast<const float4*>(src);
+    float4* d4 = reinterpret_cast<float4*>(dst);
+    const int64_t tile = static_cast<int64_t>(kCopyUnroll) * kBlock;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * tile;
+    for (int64_t base = static_cast<int64_t>(blockIdx.x) * tile + threadIdx.x; base < n4;
+         base += stride) {
+        float4 v[kCopyUnroll];
+#pragma unroll
+        for (int u = 0; u < kCopyUnroll; ++u) {
+            const int64_t k = base + static_cast<int64_t>(u) * kBlock;
+            v[u] = k < n4 ? s4[k] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < kCopyUnroll; ++u) {
+            const int64_t k = base + static_cast<int64_t>(u) * kBlock;
+            if (k < n4) d4[k] = v[u];
+        }
+    }
     const int64_t first = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    for (int64_t k = first; k < n4; k += stride)
-        reinterpret_cast<float4*>(dst)[k] = reinterpret_cast<const float4*>(src)[k];
     if (first < count - n4 * 4) dst[n4 * 4 + first] = src[n4 * 4 + first];
 }
 
@@ -836,8 +855,9 @@ hipError_t launch_loss(const float* theta, const float* h, const float* ts, int6
 hipError_t launch_copy(const float* src, float* dst, int64_t count, hipStream_t stream)
 {
     if (count <= 0) return hipSuccess;
-    const int64_t want = blocks_for(count / 4 > 0 ? count / 4 : 1);
-    const unsigned grid = static_cast<unsigned>(want < 65536 ? want : 65536);
+    const int64_t tile = static_cast<int64_t>(kCopyUnroll) * kBlock;
+    const int64_t want = (count / 4 + tile - 1) / tile;
+    const unsigned grid = static_cast<unsigned>(want < 1 ? 1 : want < 131072 ? want : 131072);
     hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(kBlock), 0, stream, src, dst, count);
     return hipGetLastError();
 }
