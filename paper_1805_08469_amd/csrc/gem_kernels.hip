@@ -5,11 +5,15 @@
 // commits to them in clock order.  theta, h and theta* are read once per
 // pass and theta written once; a worker's snapshot and moment chunks are
 // read (prefetched two commits ahead) at its first commit in the pass and
-// written at its last, held in registers in between.  Rows are read and written as 128-bit
-// accesses, consecutive lanes on consecutive chunks, so every wavefront moves
-// 1 KiB contiguous per row.  There is no contraction: the work is streaming
-// elementwise arithmetic (Philox, Box-Muller, the GEM step), bounded by HBM
-// bandwidth and VALU issue, so no MFMA is involved.
+// written at its last, held in registers in between.  Rows are read and
+// written as 128-bit accesses, consecutive lanes on consecutive chunks, so
+// every wavefront moves 1 KiB contiguous per row.  There is no contraction:
+// the work is streaming elementwise arithmetic (Philox, Box-Muller, the GEM
+// step), bounded by HBM bandwidth and VALU issue, so no MFMA is involved.
+//
+// Also here: the per-segment variant of the scale factor (a streaming step
+// kernel plus two small tree reductions per commit), the stand-alone update
+// generator, and small gather, fill, loss and copy kernels.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -315,10 +319,13 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
         for (int u = 0; u < kPrefetchDepth; ++u) {
             // Commit u reads memory iff it is the first commit of its worker
             // (u < depth); the others prefetch from the sink.
+            // With the shared moment only the snapshot row is read.
             const bool mem = u < K && (a.routes[u] & kRouteSlotMask) == kFromRing;
+            const bool mem_m = mem && !global_m;
             const int64_t lo = mem ? static_cast<int64_t>(a.worker[u]) * a.Pp + ch.off : sink_off;
             ring[u].s = *reinterpret_cast<const float4*>((mem ? a.S : a.sink_S) + lo);
-            ring[u].m = *reinterpret_cast<const float4*>((mem ? a.M : a.sink_M) + lo);
+            ring[u].m = *reinterpret_cast<const float4*>((mem_m ? a.M : a.sink_M) +
+                                                         (mem_m ? lo : sink_off));
         }
     } else {
 #pragma unroll
