@@ -110,15 +110,15 @@ def compare_rules(G, P: int = 1 << 20, T: int = 3000, every: int = 500, K: int =
     """Loss per parameter, every `every` commits, of GEM (mu = 0.9), DOWNPOUR and
     the adaptive-staleness rule (both mu = 0) on a synthetic diagonal quadratic
     (h ~ LogUniform[1e-3, 1], theta* ~ N(0, 1), noise sigma = 0.1), for n = 1..30
-    exponential-time workers and a normal (0.01) and a misspecified (0.5)
-    learning rate: the experiments of Sec. 4 on stability and misspecification,
-    run through the library."""
+    exponential-time workers and a normal (0.01), a larger (0.1) and a
+    misspecified (0.5) learning rate: the experiments of Sec. 4 on stability and
+    misspecification, run through the library."""
     from paper_1805_08469_amd.workloads import make_problem
     h, ts = make_problem(P, 1e-3, 1.0, 31)
     rules = {"gem": (G.GEM_RULE_GEM, 0.9), "downpour": (G.GEM_RULE_DOWNPOUR, 0.0),
              "adaptive": (G.GEM_RULE_ADAPTIVE, 0.0)}
     table = []
-    for lr in (0.01, 0.5):
+    for lr in (0.01, 0.1, 0.5):
         for n in (1, 5, 10, 20, 30):
             worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=n)
             for name, (rule, mu) in rules.items():
