@@ -290,13 +290,19 @@ int gem_pi_hist_read(gem_t* g, uint32_t* out, int64_t max_commits, int64_t* comm
  * theta read and written, h and theta* read (simulated runs), each distinct
  * worker's S and M rows read and written once (GLOBAL proxy: its S row, plus
  * the shared moment read and written once), and caller updates read -- 4
- * bytes per float, 2 per bfloat16. */
+ * bytes per float, 2 per bfloat16.  Under GEM_PI_SEGMENT every commit is one
+ * pass and counts 36 bytes per element (generated updates: theta, the
+ * committing and the pending worker's snapshot, the pull, M, h and theta*)
+ * or 32 / 28 (given f32 / bf16 updates, each read twice). */
 int gem_stats(gem_t* g, gem_stats_t* out);
 int gem_stats_reset(gem_t* g);
 
-/* Checkpoint: write / read theta, S, M, pull clocks, t, hyper-parameters and
- * the problem (if set) to a host file.  Load requires a handle of the same P
- * and n.  Resume is bit-exact: noise is a function of (seed, t, i). */
+/* Checkpoint: write / read theta, S, M, pull clocks, t, hyper-parameters,
+ * the problem (if set) and the segment partition (if set) to a host file.
+ * Load requires a handle of the same P and n, and checks the whole file
+ * (size, partition) before it changes any state.  Resume is bit-exact: noise
+ * is a function of (seed, t, i).  GEM_EIO for an unreadable, foreign or
+ * truncated file. */
 int gem_save(gem_t* g, const char* path);
 int gem_load(gem_t* g, const char* path);
 

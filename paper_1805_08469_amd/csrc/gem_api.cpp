@@ -973,7 +973,8 @@ int gem_schedule_make(int32_t n, int64_t T, const gem_schedule_law* law, uint64_
 
 // ---------------------------------------------------------------------------
 // Checkpoints: a small header, then theta, S rows, M rows (P floats each),
-// the pull clocks and, if set, h and theta*.
+// the pull clocks, if set h and theta*, and if set the nseg + 1 segment
+// offsets.
 // ---------------------------------------------------------------------------
 namespace {
 
@@ -985,7 +986,10 @@ struct CkptHeader {
     int64_t t;
     gem_hyperparams hp;
     gem_sim_params sp;
+    int64_t nseg;         // segments of the partition, 0 if none was set
 };
+
+constexpr char kCkptMagic[8] = {'G', 'E', 'M', 'C', 'K', 'P', 'T', '2'};
 
 int write_rows(gem_handle* g, FILE* f, const float* dev, int64_t rows, std::vector<float>& buf)
 {
@@ -1023,13 +1027,14 @@ int gem_save(gem_t* g, const char* path)
     if (!f) return GEM_EIO;
     CkptHeader hd;
     std::memset(&hd, 0, sizeof(hd));
-    std::memcpy(hd.magic, "GEMCKPT1", 8);
+    std::memcpy(hd.magic, kCkptMagic, 8);
     hd.P = g->P;
     hd.n = g->n;
     hd.have_problem = g->have_problem ? 1 : 0;
     hd.t = g->t;
     hd.hp = g->hp;
     hd.sp = g->sp;
+    hd.nseg = g->seg_host.empty() ? 0 : static_cast<int64_t>(g->seg_host.size()) - 1;
     std::vector<float> buf(static_cast<size_t>(g->P));
     int rc = std::fwrite(&hd, sizeof(hd), 1, f) == 1 ? GEM_OK : GEM_EIO;
     if (!rc) rc = write_rows(g, f, g->theta, 1, buf);
@@ -1038,6 +1043,9 @@ int gem_save(gem_t* g, const char* path)
     if (!rc && std::fwrite(g->pc.data(), sizeof(int64_t), g->pc.size(), f) != g->pc.size()) rc = GEM_EIO;
     if (!rc && g->have_problem) rc = write_rows(g, f, g->h, 1, buf);
     if (!rc && g->have_problem) rc = write_rows(g, f, g->ts, 1, buf);
+    if (!rc && hd.nseg > 0 &&
+        std::fwrite(g->seg_host.data(), sizeof(int64_t), g->seg_host.size(), f) != g->seg_host.size())
+        rc = GEM_EIO;
     if (std::fclose(f) != 0 && !rc) rc = GEM_EIO;
     return rc;
 }
@@ -1049,17 +1057,30 @@ int gem_load(gem_t* g, const char* path)
     if (!f) return GEM_EIO;
     CkptHeader hd;
     int rc = std::fread(&hd, sizeof(hd), 1, f) == 1 ? GEM_OK : GEM_EIO;
-    if (!rc && (std::memcmp(hd.magic, "GEMCKPT1", 8) != 0 || hd.P != g->P || hd.n != g->n))
+    if (!rc && (std::memcmp(hd.magic, kCkptMagic, 8) != 0 || hd.P != g->P || hd.n != g->n ||
+                hd.nseg < 0 || hd.nseg > g->P))
         rc = GEM_EIO;
     if (!rc && !valid_hp(hd.hp)) rc = GEM_EIO;
+    std::vector<int64_t> seg;
     if (!rc) {
-        // The whole file must be there before any state is overwritten.
+        // The whole file must be there, and the partition valid, before any
+        // state is overwritten.
         const int64_t rows = 1 + 2 * static_cast<int64_t>(g->n) + (hd.have_problem ? 2 : 0);
-        const int64_t want = static_cast<int64_t>(sizeof(hd)) + rows * g->P * 4 + 8 * static_cast<int64_t>(g->n);
-        if (std::fseek(f, 0, SEEK_END) != 0 || std::ftell(f) != want ||
-            std::fseek(f, static_cast<long>(sizeof(hd)), SEEK_SET) != 0)
-            rc = GEM_EIO;
+        const int64_t body = static_cast<int64_t>(sizeof(hd)) + rows * g->P * 4 + 8 * static_cast<int64_t>(g->n);
+        const int64_t want = body + (hd.nseg > 0 ? 8 * (hd.nseg + 1) : 0);
+        if (std::fseek(f, 0, SEEK_END) != 0 || std::ftell(f) != want) rc = GEM_EIO;
+        if (!rc && hd.nseg > 0) {
+            seg.resize(static_cast<size_t>(hd.nseg) + 1);
+            if (std::fseek(f, static_cast<long>(body), SEEK_SET) != 0 ||
+                std::fread(seg.data(), sizeof(int64_t), seg.size(), f) != seg.size())
+                rc = GEM_EIO;
+            if (!rc && (seg.front() != 0 || seg.back() != g->P)) rc = GEM_EIO;
+            for (size_t k = 0; !rc && k + 1 < seg.size(); ++k)
+                if (seg[k + 1] <= seg[k]) rc = GEM_EIO;
+        }
+        if (!rc && std::fseek(f, static_cast<long>(sizeof(hd)), SEEK_SET) != 0) rc = GEM_EIO;
     }
+    if (!rc && !seg.empty()) rc = build_segments(g, seg);
     if (!rc && hd.have_problem && !g->h) {
         if (hipMalloc(&g->h, static_cast<size_t>(g->Pp) * sizeof(float)) != hipSuccess ||
             hipMalloc(&g->ts, static_cast<size_t>(g->Pp) * sizeof(float)) != hipSuccess) {
@@ -1080,6 +1101,10 @@ int gem_load(gem_t* g, const char* path)
     if (!rc && hd.have_problem) rc = read_rows(g, f, g->ts, 1, buf);
     std::fclose(f);
     if (rc) return rc;
+    if (seg.empty() && !g->seg_host.empty()) {
+        GEM_HIP(hipStreamSynchronize(g->stream));
+        free_segments(g);   // the saved run used the default single segment
+    }
     g->hp = hd.hp;
     g->sp = hd.sp;
     g->have_problem = hd.have_problem != 0;
