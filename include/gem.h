@@ -232,7 +232,8 @@ int gem_clock(gem_t* g, int64_t* t);
 int gem_pull_clocks(gem_t* g, int64_t* out);
 
 /* Restart worker w as a fresh Alg. 1 Worker: m_w = 0, S[w] = theta, pull
- * clock = t (a worker that failed and came back). */
+ * clock = t (a worker that failed and came back).  With the GLOBAL proxy the
+ * shared moment belongs to the master and is kept; only the pull happens. */
 int gem_reset_worker(gem_t* g, int32_t w);
 
 /* Diagnostics (eq. 11 and eq. 22 energies, clamp count) off the timed path:

@@ -789,7 +789,8 @@ int gem_reset_worker(gem_t* g, int32_t w)
     const size_t row = static_cast<size_t>(g->Pp) * sizeof(float);
     GEM_HIP(hipMemcpyAsync(g->S + static_cast<int64_t>(w) * g->Pp, g->theta, row,
                            hipMemcpyDeviceToDevice, g->stream));
-    GEM_HIP(hipMemsetAsync(g->M + static_cast<int64_t>(w) * g->Pp, 0, row, g->stream));
+    if (g->hp.proxy_mode == GEM_PROXY_LOCAL)
+        GEM_HIP(hipMemsetAsync(g->M + static_cast<int64_t>(w) * g->Pp, 0, row, g->stream));
     g->pc[w] = g->t;
     return GEM_OK;
 }

@@ -221,22 +221,25 @@ def test_checkpoint_resume_is_bit_exact(G):
         assert np.array_equal(a, b)
 
 
-def test_reset_worker_matches_oracle(G):
-    """A worker that fails and restarts: m_w = 0, it pulls theta now (Alg. 1 Worker start-up)."""
+@pytest.mark.parametrize("proxy,w", [(0, 2), (1, 0)])
+def test_reset_worker_matches_oracle(G, proxy, w):
+    """A worker that fails and restarts: m_w = 0, it pulls theta now (Alg. 1 Worker
+    start-up).  With the shared moment (row 0 of M) only the pull happens."""
     from paper_1805_08469_amd.workloads import make_problem
     P, n = 2000, 4
     h, ts = make_problem(P, 1e-3, 1.0, 9)
     worker, tau = G.gem_schedule_make(n, 100, G.GEM_LAW_EXP, seed=9)
     st = O.State.initial(n, P)
-    ohp = O.Hyper(lr=0.01, sigma=0.1, momentum=0.9, seed=3)
-    with G.Gem(P, n) as g:
+    ohp = O.Hyper(lr=0.01, sigma=0.1, momentum=0.9, seed=3, proxy=proxy)
+    with G.Gem(P, n, _hp(G, proxy=proxy)) as g:
         g.set_quadratic(h, ts, 0.01, 0.1, 3)
         g.sim_run(worker[:50], tau[:50], 8)
         O.run(ohp, P, st, np.arange(P), h, ts, worker[:50], tau[:50])
-        assert G.gem_reset_worker(g.h, 2) == G.GEM_OK
-        st.S[2] = st.theta
-        st.M[2] = 0
-        st.pc[2] = st.t
+        assert G.gem_reset_worker(g.h, w) == G.GEM_OK
+        st.S[w] = st.theta
+        if proxy == 0:
+            st.M[w] = 0
+        st.pc[w] = st.t
         w2 = worker[50:]
         pc = st.pc.copy()
         tau2 = []
