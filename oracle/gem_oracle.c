@@ -37,6 +37,16 @@
  *   - m is per worker (a global m is a mode); kappa enters as kappa*|m|
  *     (LINEAR, appendix B, last form) or sqrt(kappa)*|m| (SQRT, appendix B,
  *     first form).
+ *
+ * What pins it (the test suite, against things other than this file):
+ * hand traces in exact dyadic arithmetic and the Psi-level cases; the n = 1
+ * reductions to SGD (bit for bit) and to the heavy-ball closed form; eqs.
+ * (12)-(13) as invariants of every element-commit; Philox against numpy's
+ * independent Philox4x64 and published known answers; ln, sin and cos
+ * exhaustively against binary64 libm; the schedule's staleness law (Sec. 1);
+ * one-element segments against the element-wise commit.  Parity unpinned:
+ * the paper prints no trajectory at n > 1, so beyond those invariants and
+ * special cases nothing but device == oracle equality pins such runs.
  */
 #include <math.h>
 #include <stdint.h>
