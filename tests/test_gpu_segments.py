@@ -81,11 +81,13 @@ def _check(out, st, tag):
     assert_parity(f"{tag} M", M, st.M)
 
 
-@pytest.mark.parametrize("kind", ["global", "ragged", "tensors", "unit"])
-@pytest.mark.parametrize("P", [300, 5003, 20_000, 600_001])
+# one-element segments only at the smaller sizes (one reduction block per element)
+PARTITIONS = [(k, P) for P in (300, 5003, 20_000, 600_001)
+              for k in ("global", "ragged", "tensors", "unit") if k != "unit" or P <= 5003]
+
+
+@pytest.mark.parametrize("kind,P", PARTITIONS)
 def test_partitions(G, kind, P):
-    if kind == "unit" and P > 5003:
-        pytest.skip("one-element segments: covered at the smaller sizes")
     n, T = 5, 40
     worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=P)
     print(f"[segments {kind}] P={P} n={n} T={T}", flush=True)
