@@ -92,7 +92,7 @@ def lib():
         L.or_run.restype = C.c_int
         L.or_run.argtypes = [C.POINTER(OracleConfig), i64p, C.c_int64, f32p, f32p,
                              f32p, f32p, f32p, i64p, C.c_int64, i32p, i32p, C.c_int64,
-                             C.c_void_p, f32p, C.POINTER(C.c_uint32)]
+                             C.c_void_p, f32p, C.POINTER(C.c_uint32), C.c_int32, i64p]
         L.or_commit_given.restype = C.c_int
         L.or_commit_given.argtypes = [C.POINTER(OracleConfig), C.c_int64, f32p, f32p, f32p,
                                       i64p, C.c_int64, i32p, i32p, C.c_int64, f32p,
@@ -254,13 +254,15 @@ class OracleError(RuntimeError):
 
 
 def run(hp: Hyper, P: int, st: State, idx, h, ts, worker, tau=None,
-        diag: bool = False, trace: bool = False, pi_hist: bool = False):
+        diag: bool = False, trace: bool = False, pi_hist: bool = False, hist_segments=None):
     """Simulated run of len(worker) commits on the element subset ``idx``.
 
     The state ``st`` (theta, S, M restricted to ``idx``) is updated in place.
     Returns (diag array or None, trace array [T, cnt, 4] of (a, pi, d, m) or None),
     plus the per-commit histograms of the applied scale factor [T, PI_BINS]
-    as a third item when ``pi_hist`` is set.
+    as a third item when ``pi_hist`` is set -- [T, nseg, PI_BINS] with one
+    histogram per segment of the global index when ``hist_segments`` (the
+    nseg + 1 offsets) is given.
     """
     idx = np.ascontiguousarray(idx, dtype=np.int64)
     cnt = idx.size
@@ -275,14 +277,20 @@ def run(hp: Hyper, P: int, st: State, idx, h, ts, worker, tau=None,
     assert st.theta.size == cnt and st.S.shape == (n, cnt) and h.size == cnt and ts.size == cnt
     dg = np.zeros(T, dtype=COMMIT_DIAG_DTYPE) if diag else None
     tr = np.zeros((T, cnt, 4), dtype=np.float32) if trace else None
-    ph = np.zeros((T, PI_BINS), dtype=np.uint32) if pi_hist else None
+    seg = None if hist_segments is None else np.ascontiguousarray(hist_segments, dtype=np.int64)
+    nseg = 0 if seg is None else seg.size - 1
+    if pi_hist:
+        shape = (T, PI_BINS) if seg is None else (T, nseg, PI_BINS)
+        ph = np.zeros(shape, dtype=np.uint32)
+    else:
+        ph = None
     cfg = hp.cfg(P, n)
     rc = lib().or_run(C.byref(cfg), _ptr(idx, C.c_int64), cnt, _ptr(h, C.c_float),
                       _ptr(ts, C.c_float), _ptr(st.theta, C.c_float), _ptr(st.S, C.c_float),
                       _ptr(st.M, C.c_float), _ptr(st.pc, C.c_int64), st.t,
                       _ptr(worker, C.c_int32), _ptr(tau_a, C.c_int32), T,
                       dg.ctypes.data if dg is not None else None,
-                      _ptr(tr, C.c_float), _ptr(ph, C.c_uint32))
+                      _ptr(tr, C.c_float), _ptr(ph, C.c_uint32), nseg, _ptr(seg, C.c_int64))
     if rc != 0:
         raise OracleError(rc)
     st.t += T

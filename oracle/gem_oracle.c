@@ -477,15 +477,21 @@ static int or_check_schedule(const or_config* c, const int64_t* pc_in, int64_t t
  * computed at its snapshot: dtheta = -eta (h (s - theta*) + sigma xi(seed, t, i)).
  * State arrays: theta[cnt], S[n*cnt], M[n*cnt] (row w at w*cnt), pc[n].
  * diag, if given, has T entries; trace, if given, has T*cnt*4 floats;
- * pi_hist, if given, has T*OR_PI_BINS counts (added to).
+ * pi_hist, if given, has T*OR_PI_BINS counts (added to); with hist_nseg > 0
+ * segments [hist_seg_off[s], hist_seg_off[s+1]) of the global index it has
+ * T*hist_nseg*OR_PI_BINS, commit-major, each element counted in its
+ * segment's histogram (the per-tensor statistics of the supplementary
+ * figures).
  */
 int or_run(const or_config* c, const int64_t* idx, int64_t cnt,
            const float* h, const float* ts,
            float* theta, float* S, float* M, int64_t* pc, int64_t t0,
            const int32_t* worker, const int32_t* tau, int64_t T,
-           or_commit_diag* diag, float* trace, uint32_t* pi_hist)
+           or_commit_diag* diag, float* trace, uint32_t* pi_hist,
+           int32_t hist_nseg, const int64_t* hist_seg_off)
 {
     if (!c || c->n <= 0 || cnt < 0 || T < 0) return OR_EINVAL;
+    if (hist_nseg < 0 || (hist_nseg > 0 && !hist_seg_off)) return OR_EINVAL;
     int rc = or_check_schedule(c, pc, t0, worker, tau, T);
     if (rc) return rc;
     const float k_eff = or_k_eff(c);
@@ -508,9 +514,15 @@ int or_run(const or_config* c, const int64_t* idx, int64_t cnt,
             float g = fmaf(h[k], diff, noise);
             float d = neg_lr * g;
             if (c->bf16) d = or_round_bf16(d);
+            uint32_t* hist = NULL;
+            if (pi_hist && hist_nseg == 0) hist = &pi_hist[j * OR_PI_BINS];
+            if (pi_hist && hist_nseg > 0) {
+                int32_t sg = 0;   /* the segment holding global index idx[k] */
+                while (sg + 1 < hist_nseg && hist_seg_off[sg + 1] <= idx[k]) ++sg;
+                hist = &pi_hist[(j * hist_nseg + sg) * OR_PI_BINS];
+            }
             or_commit_element(c, k_eff, tj, d, &theta[k], m_w, s_w, dg,
-                              trace ? &trace[(j * cnt + k) * 4] : NULL,
-                              pi_hist ? &pi_hist[j * OR_PI_BINS] : NULL);
+                              trace ? &trace[(j * cnt + k) * 4] : NULL, hist);
         }
         pc[w] = (c->pull_mode == OR_PULL_PRE) ? t : t + 1;
     }

@@ -78,20 +78,31 @@ int main(void)
         CHECK(or_schedule(N, T, 0, 0, 0, 11, c.pull_mode, worker, tau) == OR_OK);
         reset_state();
         memset(hist, 0, sizeof(hist));
-        CHECK(or_run(&c, idx, P, h, ts, theta, S, M, pc, 0, worker, tau, T, diag, trace, hist) == OR_OK);
+        CHECK(or_run(&c, idx, P, h, ts, theta, S, M, pc, 0, worker, tau, T, diag, trace, hist, 0,
+                     NULL) == OR_OK);
+        /* per-segment histograms */
+        {
+            static uint32_t seg_hist[T * 4 * OR_PI_BINS];
+            int64_t hseg[5] = {0, 1, 700, 1024, P};
+            reset_state();
+            CHECK(or_run(&c, idx, P, h, ts, theta, S, M, pc, 0, worker, tau, T, NULL, NULL,
+                         seg_hist, 4, hseg) == OR_OK);
+        }
         /* a subset run from the start */
         reset_state();
         CHECK(or_run(&c, idx + 100, 50, h + 100, ts + 100, theta, S, M, pc, 0, worker, tau, T / 2,
-                     NULL, NULL, NULL) == OR_OK);
+                     NULL, NULL, NULL, 0, NULL) == OR_OK);
     }
     /* Rejected schedules leave the state alone. */
     {
         or_config c = config(0);
         reset_state();
         int32_t bad_w[2] = {0, N};
-        CHECK(or_run(&c, idx, P, h, ts, theta, S, M, pc, 0, bad_w, NULL, 2, NULL, NULL, NULL) == OR_EWORKER);
+        CHECK(or_run(&c, idx, P, h, ts, theta, S, M, pc, 0, bad_w, NULL, 2, NULL, NULL, NULL, 0,
+                     NULL) == OR_EWORKER);
         int32_t w2[2] = {1, 1}, t2[2] = {0, 5};
-        CHECK(or_run(&c, idx, P, h, ts, theta, S, M, pc, 0, w2, t2, 2, NULL, NULL, NULL) == OR_ESTALE);
+        CHECK(or_run(&c, idx, P, h, ts, theta, S, M, pc, 0, w2, t2, 2, NULL, NULL, NULL, 0,
+                     NULL) == OR_ESTALE);
         for (int i = 0; i < P; ++i) CHECK(theta[i] == 0.0f);
     }
     /* Given updates, binary32 and bfloat16. */

@@ -452,3 +452,26 @@ def test_misspecified_learning_rate():
     assert not np.isfinite(dp[-1]) or dp[-1] > 1e6 * loss0, dp
     assert np.all(np.isfinite(gem20)) and gem20.max() < 0.5 * loss0, gem20
     assert gem20[-1] < 2 * gem1[-1], (gem20[-1], gem1[-1])
+
+
+def test_pi_histograms_per_segment():
+    """Per-segment (per-tensor) histograms: each segment's counts are the
+    whole-vector histogram of a run on that segment's indices alone (elements
+    are independent), they add up to the whole-vector histogram, and each
+    commit counts every element of a segment once."""
+    P, n, T = 3000, 4, 40
+    h, ts = _quadratic(P, 17)
+    seg = np.array([0, 1, 1023, 1024, 2500, P], dtype=np.int64)
+    w, tau = O.schedule(n, T, O.LAW_EXP, 0, 0, seed=17)
+    hp = O.Hyper(lr=0.01, sigma=0.1, momentum=0.9, seed=6)
+    _, _, whole = O.run(hp, P, O.State.initial(n, P), np.arange(P), h, ts, w, tau, pi_hist=True)
+    _, _, per = O.run(hp, P, O.State.initial(n, P), np.arange(P), h, ts, w, tau, pi_hist=True,
+                      hist_segments=seg)
+    assert per.shape == (T, seg.size - 1, O.PI_BINS)
+    assert np.array_equal(per.sum(axis=1), whole)
+    assert np.array_equal(per.sum(axis=2), np.tile(np.diff(seg), (T, 1)))
+    for k in range(seg.size - 1):
+        idx = np.arange(seg[k], seg[k + 1])
+        _, _, sub = O.run(hp, P, O.State.initial(n, idx.size), idx, h[idx], ts[idx], w, tau,
+                          pi_hist=True)
+        assert np.array_equal(per[:, k], sub)
