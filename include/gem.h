@@ -244,19 +244,6 @@ int gem_diag_enable(gem_t* g, int32_t on);
 int gem_diag_reset(gem_t* g);
 int gem_diag(gem_t* g, gem_diag_t* out);
 
-/* Histogram, for each recorded commit, of the scale factor it applied to
- * each parameter: pi for GEM (Sec. 4 follows its per-parameter median over
- * time), 1 for DOWNPOUR, 1/(tau + 1) for adaptive staleness.  Bins (on the
- * binary32 value): 0: factor <= 0 or NaN (a clamped pi is 0); 1: below 2^-20;
- * 2 + 16 o + f: 2^(o-20) (1 + f/16) <= factor < 2^(o-20) (1 + (f+1)/16) for o
- * in [0, 40), f in [0, 16); GEM_PI_BINS - 1: 2^20 and above.
- * gem_pi_hist_start allocates room for `capacity` commits (capacity >= 1) and
- * records the commits that follow, up to capacity, through the instrumented
- * kernel variant (off the timed path).  gem_pi_hist_read copies the recorded
- * histograms -- commit-major, GEM_PI_BINS uint32 counts over the P parameters
- * each -- for at most max_commits commits into out (host), sets *commits to
- * the number recorded, and stops recording.  Errors: EINVAL, ENOMEM, ESTATE
- * (read without a recording). */
 /*
  * Segments for pi_scope GEM_PI_SEGMENT: count >= 1 segments
  * [offsets[k], offsets[k+1]) of the parameter vector, offsets a host array of
@@ -283,8 +270,28 @@ int gem_diag(gem_t* g, gem_diag_t* out);
  */
 int gem_set_segments(gem_t* g, const int64_t* offsets, int32_t count);
 
+/* Histogram, for each recorded commit, of the scale factor it applied to
+ * each parameter: pi for GEM (Sec. 4 follows its per-parameter median over
+ * time), 1 for DOWNPOUR, 1/(tau + 1) for adaptive staleness.  Bins (on the
+ * binary32 value): 0: factor <= 0 or NaN (a clamped pi is 0); 1: below 2^-20;
+ * 2 + 16 o + f: 2^(o-20) (1 + f/16) <= factor < 2^(o-20) (1 + (f+1)/16) for o
+ * in [0, 40), f in [0, 16); GEM_PI_BINS - 1: 2^20 and above.
+ * gem_pi_hist_start allocates room for `capacity` commits (capacity >= 1) and
+ * records the commits that follow, up to capacity, through the instrumented
+ * kernel variant (off the timed path).  gem_pi_hist_read copies the recorded
+ * histograms -- commit-major, GEM_PI_BINS uint32 counts over the P parameters
+ * each -- for at most max_commits commits into out (host), sets *commits to
+ * the number recorded, and stops recording.  Errors: EINVAL, ENOMEM, ESTATE
+ * (read without a recording).
+ * gem_pi_hist_start_segments records one histogram per segment of the
+ * partition set by gem_set_segments (one segment if none): the per-tensor
+ * median pi of the paper's supplementary figures.  Each recorded commit is
+ * then nseg * GEM_PI_BINS counts, segment-major, and out must hold
+ * max_commits * nseg * GEM_PI_BINS.  gem_set_segments returns GEM_EINVAL
+ * while such a recording runs; gem_load ends it. */
 #define GEM_PI_BINS 643
 int gem_pi_hist_start(gem_t* g, int64_t capacity);
+int gem_pi_hist_start_segments(gem_t* g, int64_t capacity);
 int gem_pi_hist_read(gem_t* g, uint32_t* out, int64_t max_commits, int64_t* commits);
 
 /* Work counters.  alg_bytes counts, per pass over P' (P padded to 64) elements:

@@ -41,7 +41,9 @@ struct gem_handle {
     uint32_t* pi_hist = nullptr;   // [hist_cap][GEM_PI_BINS] device counts
     int64_t hist_cap = 0;
     int64_t hist_count = 0;        // commits recorded so far (may exceed hist_cap)
+    int32_t hist_rows = 1;         // histograms per commit: 1, or one per segment
     bool hist_on = false;
+    bool hist_seg = false;         // the recording is per segment of the partition
     gem_stats_t stats{};
     // Segment-norm scope: the partition (host copy) and its device tables,
     // built by gem_set_segments or, with one segment, by the first run.
@@ -289,6 +291,9 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
         }
         const bool hist = g->hist_on && g->hist_count < g->hist_cap;
         a.pi_hist = hist ? g->pi_hist : nullptr;
+        a.hist_rows = g->hist_rows;
+        a.hseg_off = g->seg_off;
+        a.hseg_grp = g->gseg;
         a.diag = g->diag_on ? g->acc : nullptr;
         a.hist_first = g->hist_count;
         a.hist_cap = g->hist_cap;
@@ -652,6 +657,7 @@ int gem_commit_batch(gem_t* g, int32_t K, const void* const* dthetas_dev, int32_
 int gem_set_segments(gem_t* g, const int64_t* offsets, int32_t count)
 {
     if (!g || !offsets || count < 1) return GEM_EINVAL;
+    if (g->hist_on && g->hist_seg) return GEM_EINVAL;   // recording per segment
     if (offsets[0] != 0 || offsets[count] != g->P) return GEM_EINVAL;
     for (int32_t k = 0; k < count; ++k)
         if (offsets[k + 1] <= offsets[k]) return GEM_EINVAL;
@@ -827,11 +833,16 @@ int gem_diag(gem_t* g, gem_diag_t* out)
     return GEM_OK;
 }
 
-int gem_pi_hist_start(gem_t* g, int64_t capacity)
+namespace {
+
+// (Re)allocate and clear room for `capacity` commits of `rows` histograms.
+int hist_begin(gem_handle* g, int64_t capacity, int32_t rows, bool per_segment)
 {
-    if (!g || capacity < 1) return GEM_EINVAL;
-    const size_t bytes = static_cast<size_t>(capacity) * GEM_PI_BINS * sizeof(uint32_t);
-    if (capacity > g->hist_cap) {
+    const size_t bytes = static_cast<size_t>(capacity) * static_cast<size_t>(rows) * GEM_PI_BINS *
+                         sizeof(uint32_t);
+    const size_t have = static_cast<size_t>(g->hist_cap) * static_cast<size_t>(g->hist_rows) *
+                        GEM_PI_BINS * sizeof(uint32_t);
+    if (!g->pi_hist || bytes > have) {
         GEM_HIP(hipStreamSynchronize(g->stream));
         (void)hipFree(g->pi_hist);
         g->pi_hist = nullptr;
@@ -839,14 +850,37 @@ int gem_pi_hist_start(gem_t* g, int64_t capacity)
         if (hipMalloc(&g->pi_hist, bytes) != hipSuccess) {
             (void)hipGetLastError();
             g->pi_hist = nullptr;
+            g->hist_on = false;
             return GEM_ENOMEM;
         }
     }
     GEM_HIP(hipMemsetAsync(g->pi_hist, 0, bytes, g->stream));
     g->hist_cap = capacity;
+    g->hist_rows = rows;
     g->hist_count = 0;
     g->hist_on = true;
+    g->hist_seg = per_segment;
     return GEM_OK;
+}
+
+}  // namespace
+
+int gem_pi_hist_start(gem_t* g, int64_t capacity)
+{
+    if (!g || capacity < 1) return GEM_EINVAL;
+    return hist_begin(g, capacity, 1, false);
+}
+
+int gem_pi_hist_start_segments(gem_t* g, int64_t capacity)
+{
+    if (!g || capacity < 1) return GEM_EINVAL;
+    if (g->seg_host.empty()) {
+        const int rc = build_segments(g, {0, g->P});
+        if (rc) return rc;
+    }
+    const int64_t nseg = static_cast<int64_t>(g->seg_host.size()) - 1;
+    if (capacity > INT64_MAX / (nseg * GEM_PI_BINS * 4)) return GEM_EINVAL;
+    return hist_begin(g, capacity, static_cast<int32_t>(nseg), true);
 }
 
 int gem_pi_hist_read(gem_t* g, uint32_t* out, int64_t max_commits, int64_t* commits)
@@ -856,7 +890,9 @@ int gem_pi_hist_read(gem_t* g, uint32_t* out, int64_t max_commits, int64_t* comm
     const int64_t recorded = std::min(g->hist_count, g->hist_cap);
     const int64_t n = std::min(recorded, max_commits);
     if (n > 0)
-        GEM_HIP(hipMemcpyAsync(out, g->pi_hist, static_cast<size_t>(n) * GEM_PI_BINS * sizeof(uint32_t),
+        GEM_HIP(hipMemcpyAsync(out, g->pi_hist,
+                               static_cast<size_t>(n) * static_cast<size_t>(g->hist_rows) *
+                                   GEM_PI_BINS * sizeof(uint32_t),
                                hipMemcpyDeviceToHost, g->stream));
     GEM_HIP(hipStreamSynchronize(g->stream));
     *commits = recorded;
@@ -1081,6 +1117,8 @@ int gem_load(gem_t* g, const char* path)
         }
         if (!rc && std::fseek(f, static_cast<long>(sizeof(hd)), SEEK_SET) != 0) rc = GEM_EIO;
     }
+    if (!rc && g->hist_on && g->hist_seg)
+        g->hist_on = false;   // the partition under a per-segment recording may change
     if (!rc && !seg.empty()) rc = build_segments(g, seg);
     if (!rc && hd.have_problem && !g->h) {
         if (hipMalloc(&g->h, static_cast<size_t>(g->Pp) * sizeof(float)) != hipSuccess ||

@@ -50,9 +50,15 @@ struct PassArgs {
     const float* h;          // [Pp]   (generated updates only)
     const float* ts;         // [Pp]   theta*
     double* diag;            // [4] accumulators, or null (diagnostic variant only)
-    uint32_t* pi_hist;       // [hist_cap][GEM_PI_BINS] or null (diagnostic variant only)
+    uint32_t* pi_hist;       // [hist_cap][hist_rows][GEM_PI_BINS] or null (diagnostic variant only)
     int64_t hist_first;      // recording index of this pass's first commit
     int64_t hist_cap;
+    // Per-segment histograms: hist_rows = number of segments, each element
+    // counted in its segment's row; hist_rows = 1: one histogram per commit.
+    const int64_t* hseg_off; // [hist_rows + 1] segment offsets (per-segment mode)
+    const int32_t* hseg_grp; // [groups] segment of each 1024-element group's first element
+    int32_t hist_rows;
+    int32_t hist_pad_;
     float* sink_S;           // [kSinkChunks * 4] target of loads/stores a step does not need
     float* sink_M;
     int64_t sink_mask;       // kSinkChunks - 1

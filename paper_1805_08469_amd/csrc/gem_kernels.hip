@@ -26,9 +26,15 @@ namespace {
 
 constexpr int kBlock = 256;
 
+// Segments a block keeps block-local histograms for (per-segment mode);
+// elements of further segments count straight into memory.
+constexpr int kHistLdsSegs = 8;
+
 struct DiagAcc {
     double ek = 0.0, proxy = 0.0, clamped = 0.0, elems = 0.0;
-    uint32_t* hist = nullptr;   // block-local histogram of the current commit (LDS)
+    uint32_t* hist = nullptr;   // block-local histograms of the current commit (LDS)
+    int32_t seg_first = 0;      // per-segment mode: the block's first segment
+    int32_t lds_rows = 1;       // histograms held in LDS
 };
 
 // Histogram bin of an applied scale factor, from its binary32 bits: 0 for
@@ -50,7 +56,7 @@ __device__ __forceinline__ int scale_bin(float x)
 template <bool FAST, bool DIAG>
 __device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float d, float s,
                                                float& th, float& m, float& snap, bool live,
-                                               DiagAcc& acc)
+                                               DiagAcc& acc, uint32_t* hist_row)
 {
     const float mn = __builtin_fmaf(a.mu, m, d);        // Alg. 1: m <- mu m + dtheta
     const float drift = th - s;                         // theta_t - s_t (eq. 16)
@@ -88,7 +94,7 @@ __device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float
         }
         snap = (a.mode & kModePrePull) ? th : th_new;
     }
-    if (DIAG && live && acc.hist) atomicAdd(&acc.hist[scale_bin(scale)], 1u);
+    if (DIAG && live && hist_row) atomicAdd(&hist_row[scale_bin(scale)], 1u);
     if (DIAG && live) {
         const double e = static_cast<double>(th_new) - static_cast<double>(s);
         const double kmd = static_cast<double>(FAST ? 1.0f : a.k_eff) * static_cast<double>(mn);
@@ -157,6 +163,7 @@ struct Chunk {
     int64_t off;     // element offset 4c
     bool active;
     bool l0, l1, l2, l3;   // elements below the true length (diagnostics)
+    int32_t sg[4];         // per-segment histograms: each element's segment
     float4 th, hh, tt;
     float4 mg;       // the shared moment (global proxy mode)
 };
@@ -237,22 +244,36 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     // the block is at commit j here (the loop is uniform), so the block-local
     // histogram is cleared, filled and flushed between barriers.
     const bool record = DIAG && acc.hist != nullptr && a.hist_first + j < a.hist_cap;
+    const int lds_bins = acc.lds_rows * GEM_PI_BINS;
     if (DIAG && acc.hist != nullptr) {
-        for (int b = threadIdx.x; b < GEM_PI_BINS; b += kBlock) acc.hist[b] = 0u;
+        for (int b = threadIdx.x; b < lds_bins; b += kBlock) acc.hist[b] = 0u;
         __syncthreads();
+    }
+    // Each element's histogram row: the block-local one of its segment, or
+    // (a segment beyond the block's LDS rows) its row of this commit in memory.
+    uint32_t* hrow[4] = {nullptr, nullptr, nullptr, nullptr};
+    if (DIAG && record) {
+        uint32_t* commit_rows = a.pi_hist + (a.hist_first + j) * a.hist_rows * GEM_PI_BINS;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int ls = ch.sg[k] - acc.seg_first;
+            hrow[k] = ls < acc.lds_rows ? acc.hist + ls * GEM_PI_BINS
+                                        : commit_rows + static_cast<int64_t>(ch.sg[k]) * GEM_PI_BINS;
+        }
     }
     StepOut r;
     r.out.m = rows.m;
-    commit_element<FAST, DIAG>(a, tau, d.x, rows.s.x, ch.th.x, r.out.m.x, r.out.s.x, ch.active && ch.l0, acc);
-    commit_element<FAST, DIAG>(a, tau, d.y, rows.s.y, ch.th.y, r.out.m.y, r.out.s.y, ch.active && ch.l1, acc);
-    commit_element<FAST, DIAG>(a, tau, d.z, rows.s.z, ch.th.z, r.out.m.z, r.out.s.z, ch.active && ch.l2, acc);
-    commit_element<FAST, DIAG>(a, tau, d.w, rows.s.w, ch.th.w, r.out.m.w, r.out.s.w, ch.active && ch.l3, acc);
+    commit_element<FAST, DIAG>(a, tau, d.x, rows.s.x, ch.th.x, r.out.m.x, r.out.s.x, ch.active && ch.l0, acc, hrow[0]);
+    commit_element<FAST, DIAG>(a, tau, d.y, rows.s.y, ch.th.y, r.out.m.y, r.out.s.y, ch.active && ch.l1, acc, hrow[1]);
+    commit_element<FAST, DIAG>(a, tau, d.z, rows.s.z, ch.th.z, r.out.m.z, r.out.s.z, ch.active && ch.l2, acc, hrow[2]);
+    commit_element<FAST, DIAG>(a, tau, d.w, rows.s.w, ch.th.w, r.out.m.w, r.out.s.w, ch.active && ch.l3, acc, hrow[3]);
 
     if (DIAG && acc.hist != nullptr) {
         __syncthreads();
         if (record) {
-            uint32_t* dst = a.pi_hist + (a.hist_first + j) * GEM_PI_BINS;
-            for (int b = threadIdx.x; b < GEM_PI_BINS; b += kBlock)
+            uint32_t* dst = a.pi_hist +
+                            ((a.hist_first + j) * a.hist_rows + acc.seg_first) * GEM_PI_BINS;
+            for (int b = threadIdx.x; b < lds_bins; b += kBlock)
                 if (acc.hist[b]) atomicAdd(&dst[b], acc.hist[b]);
         }
         __syncthreads();
@@ -333,9 +354,30 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     }
 
     DiagAcc acc;
+    ch.sg[0] = ch.sg[1] = ch.sg[2] = ch.sg[3] = 0;
     if constexpr (DIAG) {
-        __shared__ uint32_t hist_lds[GEM_PI_BINS];
-        if (a.pi_hist) acc.hist = hist_lds;
+        __shared__ uint32_t hist_lds[kHistLdsSegs * GEM_PI_BINS];
+        if (a.pi_hist) {
+            acc.hist = hist_lds;
+            if (a.hist_rows > 1) {
+                // The block's segments (uniform) and each element's segment.
+                const int64_t g_lo = static_cast<int64_t>(blockIdx.x) * kBlock * 4;
+                const int64_t g_last = (g_lo + kBlock * 4 < a.P ? g_lo + kBlock * 4 : a.P) - 1;
+                acc.seg_first = a.hseg_grp[blockIdx.x];
+                int32_t seg_last = acc.seg_first;
+                while (a.hseg_off[seg_last + 1] <= g_last) ++seg_last;
+                const int32_t rows = seg_last - acc.seg_first + 1;
+                acc.lds_rows = rows < kHistLdsSegs ? rows : kHistLdsSegs;
+                int32_t sg = acc.seg_first;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int64_t i = ch.off + k;
+                    if (ch.active && i < a.P)
+                        while (a.hseg_off[sg + 1] <= i) ++sg;
+                    ch.sg[k] = sg;
+                }
+            }
+        }
     }
     int j = 0;
     for (; j + kPrefetchDepth <= K; j += kPrefetchDepth) {

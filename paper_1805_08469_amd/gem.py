@@ -38,7 +38,7 @@ EXPORTED = (
     "gem_sim_run", "gem_read_theta", "gem_read_state", "gem_gather", "gem_clock",
     "gem_pull_clocks", "gem_reset_worker", "gem_diag_enable", "gem_diag_reset", "gem_diag",
     "gem_stats", "gem_stats_reset", "gem_save", "gem_load", "gem_sync", "gem_copy_f32",
-    "gem_pi_hist_start", "gem_pi_hist_read", "gem_set_segments",
+    "gem_pi_hist_start", "gem_pi_hist_start_segments", "gem_pi_hist_read", "gem_set_segments",
 )
 
 
@@ -119,6 +119,7 @@ def _load():
         "gem_sync": (C.c_int, [vp]),
         "gem_copy_f32": (C.c_int, [vp, vp, C.c_int64, vp]),
         "gem_pi_hist_start": (C.c_int, [vp, C.c_int64]),
+        "gem_pi_hist_start_segments": (C.c_int, [vp, C.c_int64]),
         "gem_set_segments": (C.c_int, [vp, i64p, C.c_int32]),
         "gem_pi_hist_read": (C.c_int, [vp, C.POINTER(C.c_uint32), C.c_int64, i64p]),
     }
@@ -301,11 +302,19 @@ def gem_pi_hist_start(g: int, capacity: int) -> None:
     _check(_L.gem_pi_hist_start(g, capacity), "gem_pi_hist_start")
 
 
-def gem_pi_hist_read(g: int, max_commits: int) -> np.ndarray:
-    out = np.zeros((max(max_commits, 0), GEM_PI_BINS), dtype=np.uint32)
+def gem_pi_hist_start_segments(g: int, capacity: int) -> None:
+    _check(_L.gem_pi_hist_start_segments(g, capacity), "gem_pi_hist_start_segments")
+
+
+def gem_pi_hist_read(g: int, max_commits: int, segments: int = 0) -> np.ndarray:
+    """Recorded histograms: [commits, GEM_PI_BINS], or [commits, segments,
+    GEM_PI_BINS] for a per-segment recording of that many segments."""
+    rows = max(segments, 1)
+    out = np.zeros((max(max_commits, 0), rows, GEM_PI_BINS), dtype=np.uint32)
     n = C.c_int64()
     _check(_L.gem_pi_hist_read(g, _p(out, C.c_uint32), max_commits, C.byref(n)), "gem_pi_hist_read")
-    return out[:min(n.value, max_commits)]
+    out = out[:min(n.value, max_commits)]
+    return out if segments else out[:, 0]
 
 
 def gem_sync(g: int) -> None:

@@ -276,3 +276,42 @@ def test_pi_histograms_match_oracle(G, mode):
     assert got.shape == (cap, G.GEM_PI_BINS)
     assert np.array_equal(got, hist[:cap])
     assert_parity("theta", theta, st.theta)
+
+
+# Partitions for per-segment histograms: one segment; tensors inside and across
+# the 1024-element blocks; a block holding more segments than it keeps
+# block-local histograms for (the rest count straight into memory).
+HIST_PARTITIONS = {
+    "one": lambda P: [0, P],
+    "tensors": lambda P: [0, 17, 1024, 1100, 3000, 3001, P],
+    "many_small": lambda P: sorted(set(list(range(0, 1024, 37)) + [2048, 2049, 4095, P])),
+}
+
+
+@pytest.mark.parametrize("mode", ["default", "downpour", "global_proxy"])
+@pytest.mark.parametrize("part", sorted(HIST_PARTITIONS))
+def test_pi_histograms_per_segment_match_oracle(G, mode, part):
+    """One histogram per segment (per tensor) and commit, counted exactly, in
+    the same run as the per-commit recording's oracle."""
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T, K, cap = 6000 + 7, 5, 60, 16, 50
+    seg = np.array(HIST_PARTITIONS[part](P), dtype=np.int64)
+    kw = {"default": {}, "downpour": dict(rule=1), "global_proxy": dict(proxy=1)}[mode]
+    hp = _hp(G, **kw)
+    h, ts = make_problem(P, 1e-3, 1.0, 3)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=7)
+    with G.Gem(P, n, hp) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 2)
+        g.set_segments(seg)
+        G.gem_pi_hist_start_segments(g.h, cap)
+        with pytest.raises(G.GemError):      # the partition is fixed while recording
+            g.set_segments([0, P])
+        g.sim_run(worker, tau, K)
+        got = G.gem_pi_hist_read(g.h, T, segments=seg.size - 1)
+        theta = g.theta()
+    st = O.State.initial(n, P)
+    _, _, hist = O.run(_ohp(hp, 0.01, 0.1, 2), P, st, np.arange(P), h, ts, worker, tau,
+                       pi_hist=True, hist_segments=seg)
+    assert got.shape == (cap, seg.size - 1, G.GEM_PI_BINS)
+    assert np.array_equal(got, hist[:cap])
+    assert_parity("theta", theta, st.theta)
