@@ -5,6 +5,11 @@ library ``libgem.so`` built in this package directory.  Device buffers are
 passed as integer addresses (``tensor.data_ptr()``) and streams as
 ``torch.cuda.current_stream().cuda_stream``; nothing here computes on data.
 Importing this module fails loudly if the library has not been built.
+
+The wrappers of the commit-path calls (gem_commit, gem_commit_batch,
+gem_generate, gem_sim_run, gem_reset_worker, gem_save, gem_load,
+gem_copy_f32) return the library's GEM_* code as is; the others raise
+GemError on a failed call.  The owning ``Gem`` class raises everywhere.
 """
 from __future__ import annotations
 
