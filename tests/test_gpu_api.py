@@ -181,3 +181,89 @@ def test_copy_probe(env):
         assert G.gem_copy_f32(src.data_ptr(), dst.data_ptr(), count) == G.GEM_OK
         torch.cuda.synchronize()
         assert torch.equal(src, dst)
+
+
+@pytest.mark.parametrize("source", ["host", "device"])
+def test_set_theta_restarts_from_theta0(env, source):
+    """gem_set_theta: theta = theta0, every worker pulls it (S[w] = theta0, m = 0,
+    clock and pull clocks 0), from host or device memory -- also mid-run; the
+    run that follows equals the oracle started at theta0."""
+    torch, G = env
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T = 3003, 4, 70
+    h, ts = make_problem(P, 1e-3, 1.0, 12)
+    rng = np.random.default_rng(12)
+    theta0 = rng.standard_normal(P).astype(np.float32)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=12)
+    with G.Gem(P, n) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 5)
+        g.sim_run(worker[:20], tau[:20], 8)              # state to be discarded
+        if source == "host":
+            G.gem_set_theta(g.h, theta0)
+        else:
+            dev = torch.from_numpy(theta0).cuda()
+            G.gem_set_theta(g.h, dev.data_ptr(), in_is_device=True)
+            torch.cuda.synchronize()
+        assert g.clock == 0 and np.all(g.pull_clocks() == 0)
+        assert np.array_equal(g.theta(), theta0)
+        assert np.all(g.S() == theta0[None, :]) and np.all(g.M() == 0)
+        g.sim_run(worker, tau, 8)
+        theta, S, M = g.theta(), g.S(), g.M()
+    st = O.State.initial(n, P, theta0)
+    O.run(O.Hyper(lr=0.01, sigma=0.1, seed=5), P, st, np.arange(P), h, ts, worker, tau)
+    assert_parity("theta", theta, st.theta)
+    assert_parity("S", S, st.S)
+    assert_parity("M", M, st.M)
+
+
+def test_reads_into_device_memory(env):
+    """gem_read_theta and gem_read_state write device buffers as well as host
+    ones, with the same values."""
+    import ctypes as C
+    torch, G = env
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n = 2050, 3
+    h, ts = make_problem(P, 1e-3, 1.0, 13)
+    worker, tau = G.gem_schedule_make(n, 30, G.GEM_LAW_EXP, seed=13)
+    L = G.lib()
+    with G.Gem(P, n) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 6)
+        g.sim_run(worker, tau, 8)
+        out = torch.zeros(P, dtype=torch.float32, device="cuda")
+        assert L.gem_read_theta(g.h, C.c_void_p(out.data_ptr()), 1) == G.GEM_OK
+        assert np.array_equal(out.cpu().numpy(), g.theta())
+        for which, ref in ((G.GEM_SNAPSHOT, g.S()), (G.GEM_MOMENT, g.M())):
+            for w in range(n):
+                assert L.gem_read_state(g.h, w, which, C.c_void_p(out.data_ptr()), 1) == G.GEM_OK
+                assert np.array_equal(out.cpu().numpy(), ref[w])
+        assert L.gem_read_state(g.h, n, G.GEM_SNAPSHOT, C.c_void_p(out.data_ptr()), 1) == G.GEM_EWORKER
+        assert L.gem_read_state(g.h, 0, 7, C.c_void_p(out.data_ptr()), 1) == G.GEM_EINVAL
+
+
+def test_diag_reset_restarts_the_sums(env):
+    """gem_diag_reset zeroes the energy sums and counts; what follows sums only
+    the later commits (against the oracle's per-commit diagnostics)."""
+    torch, G = env
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T = 4001, 4, 60
+    h, ts = make_problem(P, 1e-3, 1.0, 14)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=14)
+    with G.Gem(P, n) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 8)
+        G.gem_diag_enable(g.h, True)
+        g.sim_run(worker[:25], tau[:25], 8)
+        G.gem_diag_reset(g.h)
+        d0 = G.gem_diag(g.h)
+        assert (d0.sum_ek, d0.sum_proxy, d0.n_clamped, d0.n_elem_commits, d0.n_commits) == \
+               (0.0, 0.0, 0, 0, 0)
+        g.sim_run(worker[25:], tau[25:], 8)
+        d = G.gem_diag(g.h)
+    st = O.State.initial(n, P)
+    hp = O.Hyper(lr=0.01, sigma=0.1, seed=8)
+    dg, _ = O.run(hp, P, st, np.arange(P), h, ts, worker, tau, diag=True)
+    later = dg[25:]
+    assert d.n_commits == T - 25
+    assert d.n_elem_commits == P * (T - 25)
+    assert d.n_clamped == int(later["n_clamped"].sum())
+    assert d.sum_ek == pytest.approx(float(later["sum_ek"].sum()), rel=1e-9)
+    assert d.sum_proxy == pytest.approx(float(later["sum_proxy"].sum()), rel=1e-9)
