@@ -12,6 +12,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgem.so")
 SOURCES = [os.path.join(CSRC, f) for f in ("gem_kernels.hip", "gem_api.cpp")]
+# Device self-tests of the numerics (used by the test suite only).
+SELFTEST_LIB = os.path.join(HERE, "libgem_selftest.so")
+SELFTEST_SOURCES = [os.path.join(CSRC, "gem_selftest.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -22,12 +25,17 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    cmd = [HIPCC, *FLAGS, *extra, "-o", LIB + ".tmp", *SOURCES]
+def _link(out: str, sources, verbose: bool, extra) -> None:
+    cmd = [HIPCC, *FLAGS, *extra, "-o", out + ".tmp", *sources]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(out + ".tmp", out)
+
+
+def build(verbose: bool = False, extra=()) -> str:
+    _link(LIB, SOURCES, verbose, extra)
+    _link(SELFTEST_LIB, SELFTEST_SOURCES, verbose, extra)
     return LIB
 
 

@@ -2,8 +2,10 @@
 //
 // Counter-based noise and the elementwise GEM step, evaluated in IEEE binary32
 // with round-to-nearest-even in a fixed operation order: explicit fma where
-// written, correctly rounded division and square root (hipcc's default on
-// gfx950), denormals kept, no contraction (built with -ffp-contract=off).
+// written, correctly rounded division and square root (hipcc's IEEE lowering
+// on gfx950, or its core steps where the operand range leaves the rest
+// nothing to do), denormals kept, no contraction (built with
+// -ffp-contract=off).
 // Any IEEE implementation of the same steps -- in particular the host-side
 // test oracle, written separately -- produces the same bits.
 #pragma once
@@ -43,6 +45,59 @@ __host__ __device__ __forceinline__ Words4 philox10(uint32_t c0, uint32_t c1, ui
 }
 
 // ---------------------------------------------------------------------------
+// Correctly rounded division and square root for operand ranges where the
+// general IEEE sequences' range handling has nothing to do.  hipcc lowers a / b
+// to scale operands near the ends of the exponent range, refine a hardware
+// reciprocal by Newton steps with fma residual corrections, and fix up special
+// values; sqrt(x) to scale tiny x, take the hardware root and step to the
+// neighbour whose fma residual has the right sign, then handle 0 and inf.  On
+// operands with no scaling and no special value the core steps alone give the
+// same, correctly rounded, result -- which the self-test library checks
+// exhaustively over the domains used below and on a wide random sample for
+// the guarded quotient.
+// ---------------------------------------------------------------------------
+
+// a / b, correctly rounded, for normal b and a quotient well inside the
+// normal range (no scaling of either operand).
+__device__ __forceinline__ float div_rn_core(float a, float b)
+{
+    float r = __builtin_amdgcn_rcpf(b);
+    const float e = __builtin_fmaf(-b, r, 1.0f);
+    r = __builtin_fmaf(e, r, r);                    // refined reciprocal
+    float q = a * r;
+    const float e2 = __builtin_fmaf(-b, q, a);
+    q = __builtin_fmaf(e2, r, q);
+    const float e3 = __builtin_fmaf(-b, q, a);
+    return __builtin_fmaf(e3, r, q);
+}
+
+// sqrt(x), correctly rounded, for x = +0 or normal x (no scaling).
+__device__ __forceinline__ float sqrt_rn_core(float x)
+{
+    const float y = __builtin_amdgcn_sqrtf(x);
+    const float dn = __uint_as_float(__float_as_uint(y) - 1u);
+    const float up = __uint_as_float(__float_as_uint(y) + 1u);
+    const float r_dn = __builtin_fmaf(-dn, y, x);
+    const float r_up = __builtin_fmaf(-up, y, x);
+    float r = (r_dn <= 0.0f) ? dn : y;
+    r = (r_up > 0.0f) ? up : r;
+    return r;
+}
+
+// num / den, correctly rounded for every input: the core steps when both
+// magnitudes lie in [2^-60, 2^60] (quotient in [2^-120, 2^120]), the general
+// division otherwise (zero, tiny, huge, infinite or NaN operands).
+__device__ __forceinline__ float div_rn(float num, float den)
+{
+    const float an = __builtin_fabsf(num), ad = __builtin_fabsf(den);
+    const bool core = an >= 0x1p-60f && an <= 0x1p60f && ad >= 0x1p-60f && ad <= 0x1p60f;
+    float q;
+    if (core) q = div_rn_core(num, den);
+    else q = num / den;
+    return q;
+}
+
+// ---------------------------------------------------------------------------
 // Natural logarithm of u = k * 2^-24 for an integer k in [1, 2^24] (the Box-
 // Muller radius argument).  u = 2^e f with f in (sqrt(1/2), sqrt(2)];
 // ln f = 2 atanh((f-1)/(f+1)) by its series to the s^9 term (Abramowitz &
@@ -58,7 +113,9 @@ __device__ __forceinline__ float ln_of_unit(float u)
     const uint32_t fbits = mant | (upper ? 0x3F000000u : 0x3F800000u);
     e += upper ? 1 : 0;
     const float f = __uint_as_float(fbits);
-    const float s = (f - 1.0f) / (f + 1.0f);
+    // f - 1 is exact and 0 or at least 2^-24 in magnitude, f + 1 in (1.7, 2.5):
+    // the division needs no scaling.
+    const float s = div_rn_core(f - 1.0f, f + 1.0f);
     const float z = s * s;
     float p = 1.0f / 9.0f;
     p = __builtin_fmaf(p, z, 1.0f / 7.0f);
@@ -112,7 +169,8 @@ __device__ __forceinline__ void sincos_of_turn(uint32_t k, float& sn, float& cs)
 __device__ __forceinline__ void box_muller(uint32_t xa, uint32_t xb, float& zc, float& zs)
 {
     const float u1 = static_cast<float>((xa >> 8) + 1u) * 0x1p-24f;
-    const float r = __builtin_sqrtf(-2.0f * ln_of_unit(u1));
+    // -2 ln u1 is +0 (u1 = 1) or at least 1.1e-7: no scaling.
+    const float r = sqrt_rn_core(-2.0f * ln_of_unit(u1));
     float sn, cs;
     sincos_of_turn(xb >> 8, sn, cs);
     zc = r * cs;

@@ -67,7 +67,7 @@ __device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float
     if (FAST) {
         const float num = __builtin_fabsf(mn) - __builtin_fabsf(drift);
         const float den = __builtin_fabsf(d) + a.eps;
-        pi_raw = num / den;                             // eq. 18 / Alg. 1
+        pi_raw = div_rn(num, den);                      // eq. 18 / Alg. 1
         const float pi = (pi_raw > 0.0f) ? pi_raw : 0.0f;
         th_new = __builtin_fmaf(pi, d, th);             // eq. 3
         snap = th_new;
@@ -86,7 +86,7 @@ __device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float
                                                       : __builtin_fabsf(mn);
             const float num = km - __builtin_fabsf(drift);
             const float den = __builtin_fabsf(d) + a.eps;
-            pi_raw = num / den;
+            pi_raw = div_rn(num, den);
             const float pi = (a.mode & kModeLiteralPi) ? pi_raw
                                                        : ((pi_raw > 0.0f) ? pi_raw : 0.0f);
             th_new = __builtin_fmaf(pi, d, th);
