@@ -263,8 +263,10 @@ int gem_diag(gem_t* g, gem_diag_t* out);
  * binary32; segments of one element give element-wise GEM bit for bit.
  * Each commit is one streaming launch plus two small reduction launches (a
  * commit's pi needs every element of its segment first), so commits are not
- * fused.  Diagnostics and pi histograms are element-wise only: a commit or
- * run with either enabled returns GEM_EINVAL under this scope.
+ * fused.  pi histograms record each segment's factor once per element (one
+ * bin per segment holding its size).  The energy diagnostics are
+ * element-wise only: a commit or run with them enabled returns GEM_EINVAL
+ * under this scope.
  * The offsets are copied; the call may be made at any time between commits.
  * GEM_EINVAL for a malformed table.
  */

@@ -456,8 +456,14 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
         GEM_HIP(gemk::launch_seg_step(a, src, bf16_out, g->stream));
         GEM_HIP(gemk::launch_seg_blocks(g->part, g->npart, g->part_off, g->seg_off, g->pair_seg,
                                         g->pair_blk, g->nsup, g->sup, g->sup_off, g->stream));
+        // Histogram recording: this commit's rows, while there is room.
+        uint32_t* hist = nullptr;
+        if (g->hist_on && g->hist_count < g->hist_cap)
+            hist = g->pi_hist + g->hist_count * g->hist_rows * GEM_PI_BINS;
         GEM_HIP(gemk::launch_seg_reduce(g->sup, g->nsup, g->sup_off, nseg, g->pi_seg, k_eff,
-                                        g->hp.eps, literal, g->stream));
+                                        g->hp.eps, literal, g->seg_off, hist, g->hist_seg,
+                                        g->stream));
+        if (g->hist_on) g->hist_count += 1;
         g->pc[w] = next_pull(g, t);
         g->t += 1;
         g->stats.commits += 1;
@@ -646,7 +652,7 @@ int gem_commit_batch(gem_t* g, int32_t K, const void* const* dthetas_dev, int32_
     if (rc) return rc;
     const Source src = dtype == GEM_F32 ? Source::GivenF32 : Source::GivenBF16;
     if (g->hp.pi_scope == GEM_PI_SEGMENT) {
-        if (g->diag_on || g->hist_on) return GEM_EINVAL;
+        if (g->diag_on) return GEM_EINVAL;
         return run_segments(g, worker_ids, K, src, dthetas_dev, false);
     }
     std::vector<Pass> passes;
@@ -693,7 +699,7 @@ int gem_sim_run(gem_t* g, const int32_t* worker, const int32_t* tau, int64_t T, 
     int rc = check_sequence(g, worker, tau, T);
     if (rc) return rc;
     if (g->hp.pi_scope == GEM_PI_SEGMENT) {
-        if (g->diag_on || g->hist_on) return GEM_EINVAL;
+        if (g->diag_on) return GEM_EINVAL;
         return run_segments(g, worker, T, Source::Generated, nullptr,
                             g->sp.update_dtype == GEM_BF16);
     }

@@ -134,6 +134,7 @@ hipError_t launch_seg_blocks(const double* part, int64_t npart, const int64_t* p
                              const int64_t* sup_off, hipStream_t stream);
 hipError_t launch_seg_reduce(const double* sup, int64_t nsup, const int64_t* sup_off,
                              int32_t nseg, float* pi_seg, float k_eff, float eps, bool literal,
+                             const int64_t* seg_off, uint32_t* hist, bool hist_per_seg,
                              hipStream_t stream);
 hipError_t launch_generate(const float* S_w, const float* h, const float* ts, void* out,
                            bool bf16, int64_t P, uint32_t t, uint32_t key0, uint32_t key1,

@@ -630,7 +630,10 @@ __global__ __launch_bounds__(64) void seg_reduce_kernel(const double* __restrict
                                                         int64_t nsup,
                                                         const int64_t* __restrict__ sup_off,
                                                         float* __restrict__ pi_seg,
-                                                        float k_eff, float eps, int32_t literal)
+                                                        float k_eff, float eps, int32_t literal,
+                                                        const int64_t* __restrict__ seg_off,
+                                                        uint32_t* __restrict__ hist,
+                                                        int32_t hist_per_seg)
 {
     const int32_t seg = blockIdx.x;
     const int64_t q0 = sup_off[seg], q1 = sup_off[seg + 1];
@@ -659,6 +662,12 @@ __global__ __launch_bounds__(64) void seg_reduce_kernel(const double* __restrict
     float pi = num / den;
     if (!literal) pi = (pi > 0.0f) ? pi : 0.0f;
     pi_seg[seg] = pi;
+    // Recording: every element of the segment takes this factor, so its
+    // histogram entry is one bin holding the segment's size.
+    if (hist) {
+        uint32_t* row = hist + (hist_per_seg ? static_cast<int64_t>(seg) * GEM_PI_BINS : 0);
+        atomicAdd(&row[scale_bin(pi)], static_cast<uint32_t>(seg_off[seg + 1] - seg_off[seg]));
+    }
 }
 
 template <bool BF16>
@@ -855,10 +864,12 @@ hipError_t launch_seg_blocks(const double* part, int64_t npart, const int64_t* p
 
 hipError_t launch_seg_reduce(const double* sup, int64_t nsup, const int64_t* sup_off,
                              int32_t nseg, float* pi_seg, float k_eff, float eps, bool literal,
+                             const int64_t* seg_off, uint32_t* hist, bool hist_per_seg,
                              hipStream_t stream)
 {
     hipLaunchKernelGGL(seg_reduce_kernel, dim3(static_cast<unsigned>(nseg)), dim3(64), 0, stream,
-                       sup, nsup, sup_off, pi_seg, k_eff, eps, literal ? 1 : 0);
+                       sup, nsup, sup_off, pi_seg, k_eff, eps, literal ? 1 : 0, seg_off, hist,
+                       hist_per_seg ? 1 : 0);
     return hipGetLastError();
 }
 

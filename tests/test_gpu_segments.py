@@ -202,6 +202,38 @@ def test_given_updates(G, dtype):
     _check(out, st, f"given {dtype}")
 
 
+@pytest.mark.parametrize("per_segment", [False, True])
+def test_pi_histograms(G, per_segment):
+    """Histograms under the segment scope: each commit counts every element of
+    a segment in the bin of that segment's factor (the oracle's pi per segment
+    and commit, binned by the oracle)."""
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T, cap = 7000, 4, 30, 25
+    seg = _partition("tensors", P)
+    nseg = seg.size - 1
+    h, ts = make_problem(P, 1e-3, 1.0, 3)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=3)
+    hp = _hp(G)
+    with G.Gem(P, n, hp) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 7)
+        g.set_segments(seg)
+        if per_segment:
+            G.gem_pi_hist_start_segments(g.h, cap)
+        else:
+            G.gem_pi_hist_start(g.h, cap)
+        g.sim_run(worker, tau, 8)
+        got = G.gem_pi_hist_read(g.h, T, segments=nseg if per_segment else 0)
+    st = O.State.initial(n, P)
+    pi, _ = O.run_segments(_ohp(hp, 0.01, 0.1, 7), st, seg, worker, tau, h=h, ts=ts, pi=True)
+    bins = O.pi_bin(pi)                                   # [T, nseg]
+    size = np.diff(seg)
+    want = np.zeros((cap, nseg if per_segment else 1, G.GEM_PI_BINS), dtype=np.uint32)
+    for j in range(cap):
+        for k in range(nseg):
+            want[j, k if per_segment else 0, bins[j, k]] += size[k]
+    assert np.array_equal(got, want if per_segment else want[:, 0])
+
+
 def test_rejections(G):
     P, n = 1000, 2
     hp = _hp(G)
