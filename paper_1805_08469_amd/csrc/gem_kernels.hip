@@ -53,6 +53,9 @@ __device__ __forceinline__ int scale_bin(float x)
 // One element of one commit.  th and m are the element's central value and
 // the committing worker's moment (in/out); s is its snapshot; d the update.
 // snap receives the value the worker's snapshot takes after this commit.
+// FAST: the default rule (GEM, CLAMP0, kappa_eff = 1, post-commit pull) with
+// no runtime mode tests; otherwise every mode is read from a.mode.
+// hist_row: the histogram row this element's factor counts in, or null.
 template <bool FAST, bool DIAG>
 __device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float d, float s,
                                                float& th, float& m, float& snap, bool live,
@@ -421,10 +424,12 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
 // ---------------------------------------------------------------------------
 // Segment-norm scale factors (one pi per segment of the parameter vector).
 // A commit's pi needs sums of squares over whole segments, so each commit is
-// split in two launches: the step kernel starts commit t (forms d, m and the
-// drift, stores m and d, writes group sums of squares) and the reduction
-// turns the group sums into one pi per segment; the next step kernel applies
-// those factors (and the pull) before starting the next commit.
+// split in three launches: the step kernel starts commit t (forms d, m and
+// the drift, stores m, writes each 1024-index group's tree sums of squares),
+// seg_blocks_kernel adds the group sums of each 2^18-index block by the same
+// tree, and seg_reduce_kernel adds the block sums in order and forms one pi
+// per segment.  The next step kernel applies those factors (and the pull)
+// before starting the next commit, generating the pending update again.
 // ---------------------------------------------------------------------------
 
 __device__ __forceinline__ float4 f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
