@@ -39,10 +39,16 @@ COUNTERS_FILES = {
 
 
 def kernel_hash() -> str:
+    """Hash of the kernel sources' code: comments and blank lines removed, so
+    an edit of comments alone keeps counter summaries taken on the same code."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_1805_08469_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_1805_08469_amd", "csrc", f)) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)      # block comments
+        text = re.sub(r"//[^\n]*", "", text)                    # line comments
+        code = "\n".join(line.rstrip() for line in text.splitlines() if line.strip())
+        h.update(code.encode())
     return h.hexdigest()[:16]
 
 
