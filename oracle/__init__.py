@@ -103,7 +103,7 @@ def lib():
         L.or_run_segments.restype = C.c_int
         L.or_run_segments.argtypes = [C.POINTER(OracleConfig), C.c_int32, i64p, f32p, f32p,
                                       f32p, f32p, f32p, i64p, C.c_int64, i32p, i32p, C.c_int64,
-                                      f32p, C.POINTER(C.c_uint16), f32p, f32p]
+                                      f32p, C.POINTER(C.c_uint16), f32p, f32p, C.c_void_p]
         L.or_pi_bin.restype = C.c_int
         L.or_pi_bin.argtypes = [C.c_float]
         L.or_pi_bin_array.argtypes = [f32p, i32p, C.c_int64]
@@ -339,14 +339,15 @@ def sumsq(x, lo: int = 0, hi: int | None = None) -> float:
 
 
 def run_segments(hp: Hyper, st: State, seg_off, worker, tau=None, h=None, ts=None, d=None,
-                 pi: bool = False, trace: bool = False):
+                 pi: bool = False, trace: bool = False, diag: bool = False):
     """Commits with one scale factor per segment [seg_off[k], seg_off[k+1]) of the
     parameter vector (norms over the segment in eq. 18; see or_run_segments).
 
     Updates are generated at the snapshots from (h, ts) as in ``run`` (on all P
     elements) when ``d`` is None, else given as d[T, P] (float32, or uint16
     bf16 bit patterns).  Returns (pi [T, nseg] or None, trace [T, P, 3] of
-    (a, d, m) or None).
+    (a, d, m) or None), plus the per-commit energy diagnostics as a third
+    item when ``diag`` is set.
     """
     n, P = st.S.shape
     seg_off = np.ascontiguousarray(seg_off, dtype=np.int64)
@@ -370,17 +371,18 @@ def run_segments(hp: Hyper, st: State, seg_off, worker, tau=None, h=None, ts=Non
         assert h.size == P and ts.size == P
     po = np.zeros((T, nseg), dtype=np.float32) if pi else None
     tr = np.zeros((T, P, 3), dtype=np.float32) if trace else None
+    dg = np.zeros(T, dtype=COMMIT_DIAG_DTYPE) if diag else None
     cfg = hp.cfg(P, n)
     rc = lib().or_run_segments(C.byref(cfg), nseg, _ptr(seg_off, C.c_int64), _ptr(h, C.c_float),
                                _ptr(ts, C.c_float), _ptr(st.theta, C.c_float),
                                _ptr(st.S, C.c_float), _ptr(st.M, C.c_float),
                                _ptr(st.pc, C.c_int64), st.t, _ptr(worker, C.c_int32),
                                _ptr(tau_a, C.c_int32), T, df, db, _ptr(po, C.c_float),
-                               _ptr(tr, C.c_float))
+                               _ptr(tr, C.c_float), dg.ctypes.data if dg is not None else None)
     if rc != 0:
         raise OracleError(rc)
     st.t += T
-    return po, tr
+    return (po, tr, dg) if diag else (po, tr)
 
 
 def loss(theta, h, ts) -> float:

@@ -623,12 +623,16 @@ static float or_norm(const float* x, int64_t lo, int64_t hi)
  * Updates are generated at the snapshots as in or_run when d and db are both
  * NULL, else given as in or_commit_given.  GEM rule only.  pi_out, if given,
  * receives the applied pi of every segment of every commit (T * nseg);
- * trace, if given, (a, d, m) of every element of every commit (T * P * 3).
+ * trace, if given, (a, d, m) of every element of every commit (T * P * 3);
+ * diag, if given, the energies of each commit as in or_run (T entries), with
+ * n_clamped counting the elements of segments whose raw pi was negative or
+ * NaN.
  */
 int or_run_segments(const or_config* c, int32_t nseg, const int64_t* seg_off,
                     const float* h, const float* ts, float* theta, float* S, float* M,
                     int64_t* pc, int64_t t0, const int32_t* worker, const int32_t* tau,
-                    int64_t T, const float* d, const uint16_t* db, float* pi_out, float* trace)
+                    int64_t T, const float* d, const uint16_t* db, float* pi_out, float* trace,
+                    or_commit_diag* diag)
 {
     if (!c || c->n <= 0 || c->P < 0 || T < 0 || nseg < 1 || !seg_off) return OR_EINVAL;
     if (c->rule != OR_RULE_GEM) return OR_EINVAL;
@@ -651,6 +655,8 @@ int or_run_segments(const or_config* c, int32_t nseg, const int64_t* seg_off,
         const int64_t mrow = (c->proxy == OR_PROXY_GLOBAL) ? 0 : w;
         float* s_row = &S[(int64_t)w * P];
         float* m_row = &M[mrow * P];
+        or_commit_diag* dg = diag ? &diag[j] : NULL;
+        if (dg) memset(dg, 0, sizeof(*dg));
         /* The update, the refreshed first moment (Alg. 1, eq. 23) and the
          * drift theta_t - s_t (eq. 16), element by element. */
         for (int64_t i = 0; i < P; ++i) {
@@ -680,12 +686,22 @@ int or_run_segments(const or_config* c, int32_t nseg, const int64_t* seg_off,
             /* Eq. (18) with norms over the segment. */
             float num = k_eff * or_norm(mv, lo, hi) - or_norm(av, lo, hi);
             float den = or_norm(dv, lo, hi) + c->eps;
-            float pi = num / den;
+            const float pi_raw = num / den;
+            float pi = pi_raw;
             if (c->pi_mode == OR_PI_CLAMP0) pi = (pi > 0.0f) ? pi : 0.0f;
             if (pi_out) pi_out[j * nseg + k] = pi;
+            if (dg && !(pi_raw >= 0.0f)) dg->n_clamped += hi - lo;
             for (int64_t i = lo; i < hi; ++i) {
                 const float th_old = theta[i];
                 const float th_new = fmaf(pi, dv[i], th_old);   /* eq. (3) */
+                if (dg) {
+                    /* E_k (eq. 11) against the committing worker's snapshot
+                     * and the proxy energy (eq. 22), as in or_commit_element. */
+                    const double e = (double)th_new - (double)s_row[i];
+                    const double km = (double)k_eff * (double)mv[i];
+                    dg->sum_ek += 0.5 * e * e;
+                    dg->sum_proxy += 0.5 * km * km;
+                }
                 m_row[i] = mv[i];
                 s_row[i] = (c->pull_mode == OR_PULL_PRE) ? th_old : th_new;
                 theta[i] = th_new;

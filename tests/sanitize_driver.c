@@ -124,10 +124,10 @@ int main(void)
         static float pi_out[8 * 3];
         reset_state();
         CHECK(or_run_segments(&c, 3, seg, NULL, NULL, theta, S, M, pc, 0, worker, tau, 8, d, NULL,
-                              pi_out, NULL) == OR_OK);
+                              pi_out, NULL, diag) == OR_OK);
         reset_state();
         CHECK(or_run_segments(&c, 3, seg, NULL, NULL, theta, S, M, pc, 0, worker, tau, 8, NULL, db,
-                              NULL, NULL) == OR_OK);
+                              NULL, NULL, NULL) == OR_OK);
     }
     /* Segment norms with generated updates, every supported mode. */
     for (int mode = 0; mode <= 7; ++mode) {
@@ -139,18 +139,18 @@ int main(void)
         static float tr3[40 * P * 3];
         reset_state();
         CHECK(or_run_segments(&c, 5, seg, h, ts, theta, S, M, pc, 0, worker, tau, 40, NULL, NULL,
-                              pi_out, tr3) == OR_OK);
+                              pi_out, tr3, diag) == OR_OK);
     }
     {
         or_config c = config(0);
         int64_t bad1[3] = {0, 0, P}, bad2[2] = {1, P}, good[2] = {0, P};
         CHECK(or_run_segments(&c, 2, bad1, h, ts, theta, S, M, pc, 0, worker, tau, 1, NULL, NULL,
-                              NULL, NULL) == OR_EINVAL);
+                              NULL, NULL, NULL) == OR_EINVAL);
         CHECK(or_run_segments(&c, 1, bad2, h, ts, theta, S, M, pc, 0, worker, tau, 1, NULL, NULL,
-                              NULL, NULL) == OR_EINVAL);
+                              NULL, NULL, NULL) == OR_EINVAL);
         c.rule = OR_RULE_DOWNPOUR;
         CHECK(or_run_segments(&c, 1, good, h, ts, theta, S, M, pc, 0, worker, tau, 1, NULL, NULL,
-                              NULL, NULL) == OR_EINVAL);
+                              NULL, NULL, NULL) == OR_EINVAL);
     }
     CHECK(or_sumsq(h, 5, 5) == 0.0);
     CHECK(or_loss(theta, h, ts, P) >= 0.0);

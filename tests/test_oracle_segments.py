@@ -165,3 +165,17 @@ def test_bad_segments_rejected():
     with pytest.raises(O.OracleError):
         O.run_segments(O.Hyper(rule=O.RULE_DOWNPOUR), O.State.initial(n, P), [0, P], w,
                        h=h, ts=ts)
+
+
+def test_unit_segments_diagnostics_equal_elementwise():
+    """The energy diagnostics of a one-element-segment run equal the
+    element-wise run's, commit by commit (same terms, same order)."""
+    P, n, T = 1200, 4, 50
+    h, ts = _problem(P, 21)
+    hp = O.Hyper(lr=0.01, sigma=0.1, seed=4)
+    w, tau = O.schedule(n, T, O.LAW_EXP, 0, 0, seed=21)
+    dg, _ = O.run(hp, P, O.State.initial(n, P), np.arange(P), h, ts, w, tau, diag=True)
+    _, _, dgs = O.run_segments(hp, O.State.initial(n, P), np.arange(P + 1), w, tau, h=h, ts=ts,
+                               diag=True)
+    assert np.array_equal(dg, dgs)
+    assert dg["n_clamped"].sum() > 0
