@@ -264,9 +264,8 @@ int gem_diag(gem_t* g, gem_diag_t* out);
  * Each commit is one streaming launch plus two small reduction launches (a
  * commit's pi needs every element of its segment first), so commits are not
  * fused.  pi histograms record each segment's factor once per element (one
- * bin per segment holding its size).  The energy diagnostics are
- * element-wise only: a commit or run with them enabled returns GEM_EINVAL
- * under this scope.
+ * bin per segment holding its size); the diagnostics count the elements of
+ * segments whose raw pi was negative or NaN as clamped.
  * The offsets are copied; the call may be made at any time between commits.
  * GEM_EINVAL for a malformed table.
  */

@@ -436,6 +436,8 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
     a.mu = g->hp.momentum;
     const float k_eff = kappa_eff(g->hp);
     const bool literal = g->hp.pi_mode == GEM_PI_LITERAL;
+    a.k_eff = k_eff;
+    a.diag = g->diag_on ? g->acc : nullptr;
     // Bytes per element-commit the launches move: theta read and written, the
     // committing worker's snapshot read and its pull written, the moment read
     // and written; generated updates read h and theta* and the pending
@@ -449,6 +451,7 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
         a.start = 1;
         a.w_prev = j > 0 ? worker[j - 1] : 0;
         a.w_cur = w;
+        a.m_row_prev = a.m_row;
         a.m_row = g->hp.proxy_mode == GEM_PROXY_GLOBAL ? 0 : w;
         a.t = static_cast<uint32_t>(t);
         a.upd_prev = (upd && j > 0) ? upd[j - 1] : nullptr;
@@ -462,8 +465,9 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
             hist = g->pi_hist + g->hist_count * g->hist_rows * GEM_PI_BINS;
         GEM_HIP(gemk::launch_seg_reduce(g->sup, g->nsup, g->sup_off, nseg, g->pi_seg, k_eff,
                                         g->hp.eps, literal, g->seg_off, hist, g->hist_seg,
-                                        g->stream));
+                                        a.diag, g->stream));
         if (g->hist_on) g->hist_count += 1;
+        if (g->diag_on) g->diag_commits += 1;
         g->pc[w] = next_pull(g, t);
         g->t += 1;
         g->stats.commits += 1;
@@ -474,6 +478,7 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
     a.start = 0;
     a.t = static_cast<uint32_t>(g->t);
     a.w_prev = worker[T - 1];
+    a.m_row_prev = a.m_row;
     a.upd_prev = upd ? upd[T - 1] : nullptr;
     a.upd_cur = nullptr;
     GEM_HIP(gemk::launch_seg_step(a, src, bf16_out, g->stream));
@@ -652,7 +657,6 @@ int gem_commit_batch(gem_t* g, int32_t K, const void* const* dthetas_dev, int32_
     if (rc) return rc;
     const Source src = dtype == GEM_F32 ? Source::GivenF32 : Source::GivenBF16;
     if (g->hp.pi_scope == GEM_PI_SEGMENT) {
-        if (g->diag_on) return GEM_EINVAL;
         return run_segments(g, worker_ids, K, src, dthetas_dev, false);
     }
     std::vector<Pass> passes;
@@ -699,7 +703,6 @@ int gem_sim_run(gem_t* g, const int32_t* worker, const int32_t* tau, int64_t T, 
     int rc = check_sequence(g, worker, tau, T);
     if (rc) return rc;
     if (g->hp.pi_scope == GEM_PI_SEGMENT) {
-        if (g->diag_on) return GEM_EINVAL;
         return run_segments(g, worker, T, Source::Generated, nullptr,
                             g->sp.update_dtype == GEM_BF16);
     }

@@ -113,7 +113,10 @@ struct SegArgs {
     int32_t w_prev;           // worker of the pending commit
     int32_t w_cur;            // worker of commit t
     int32_t m_row;            // row of M that commit t refreshes
+    int32_t m_row_prev;       // row of M the pending commit refreshed (diagnostics)
     int32_t pre_pull;         // the snapshot keeps the pre-commit theta
+    double* diag;             // [4] accumulators, or null (diagnostic variant)
+    float k_eff;              // kappa as it multiplies the moment (diagnostics)
     uint32_t t;               // clock of commit t; the pending commit's is t - 1
     uint32_t key0, key1;
     float neg_lr, sigma, mu;
@@ -135,7 +138,7 @@ hipError_t launch_seg_blocks(const double* part, int64_t npart, const int64_t* p
 hipError_t launch_seg_reduce(const double* sup, int64_t nsup, const int64_t* sup_off,
                              int32_t nseg, float* pi_seg, float k_eff, float eps, bool literal,
                              const int64_t* seg_off, uint32_t* hist, bool hist_per_seg,
-                             hipStream_t stream);
+                             double* diag, hipStream_t stream);
 hipError_t launch_generate(const float* S_w, const float* h, const float* ts, void* out,
                            bool bf16, int64_t P, uint32_t t, uint32_t key0, uint32_t key1,
                            float neg_lr, float sigma, hipStream_t stream);

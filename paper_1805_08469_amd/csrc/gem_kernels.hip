@@ -460,7 +460,7 @@ __device__ __forceinline__ double block_tree_sum(double v, double* lds)
     return r;
 }
 
-template <Source SRC, bool BF16>
+template <Source SRC, bool BF16, bool DIAG>
 __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
 {
     static_assert(kBlock * 4 == kSegGroup, "one block per group of sums");
@@ -478,13 +478,15 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
         hv = f4(a.h + off);
         tv = f4(a.ts + off);
     }
+    double ek = 0.0, proxy = 0.0;   // diagnostic variant: energies of the pending commit
     if (a.apply && active) {
         // The pending commit's update: the caller's, or generated again at
         // the worker's snapshot, which its pull below replaces.
         float4 d;
         float* srow = a.S + static_cast<int64_t>(a.w_prev) * a.Pp + off;
+        float4 sp = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (SRC == Source::Generated || DIAG) sp = f4(srow);
         if (SRC == Source::Generated) {
-            const float4 sp = f4(srow);
             const float4 z = normals4(static_cast<uint64_t>(c), a.t - 1u, a.key0, a.key1);
             d.x = stale_update<BF16>(a.neg_lr, a.sigma, sp.x, hv.x, tv.x, z.x);
             d.y = stale_update<BF16>(a.neg_lr, a.sigma, sp.y, hv.y, tv.y, z.y);
@@ -504,6 +506,28 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
         if (off + 2 < a.P) th.z = __builtin_fmaf(factor(off + 2), d.z, th.z);
         if (off + 3 < a.P) th.w = __builtin_fmaf(factor(off + 3), d.w, th.w);
         *reinterpret_cast<float4*>(srow) = pick(a.pre_pull, th_old, th);
+        if (DIAG) {
+            // E_k against the worker's snapshot (eq. 11) and the proxy energy
+            // (eq. 22) of the pending commit, whose moment is already stored.
+            const float4 mp = f4(a.M + static_cast<int64_t>(a.m_row_prev) * a.Pp + off);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                if (off + k < a.P) {
+                    const double e = static_cast<double>(lane(th, k)) - static_cast<double>(lane(sp, k));
+                    const double km = static_cast<double>(a.k_eff) * static_cast<double>(lane(mp, k));
+                    ek += 0.5 * e * e;
+                    proxy += 0.5 * km * km;
+                }
+            }
+        }
+    }
+    if (DIAG && a.apply) {   // uniform: every thread of the block takes part
+        const double bek = block_tree_sum(ek, lds[0]);
+        const double bpr = block_tree_sum(proxy, lds[1]);
+        if (threadIdx.x == 0) {
+            atomicAdd(&a.diag[0], bek);
+            atomicAdd(&a.diag[1], bpr);
+        }
     }
     if (!a.start) {
         if (active) *reinterpret_cast<float4*>(a.theta + off) = th;
@@ -638,7 +662,7 @@ __global__ __launch_bounds__(64) void seg_reduce_kernel(const double* __restrict
                                                         float k_eff, float eps, int32_t literal,
                                                         const int64_t* __restrict__ seg_off,
                                                         uint32_t* __restrict__ hist,
-                                                        int32_t hist_per_seg)
+                                                        int32_t hist_per_seg, double* diag)
 {
     const int32_t seg = blockIdx.x;
     const int64_t q0 = sup_off[seg], q1 = sup_off[seg + 1];
@@ -664,9 +688,14 @@ __global__ __launch_bounds__(64) void seg_reduce_kernel(const double* __restrict
     const float nd = static_cast<float>(sqrt(sd));
     const float num = k_eff * nm - na;
     const float den = nd + eps;
-    float pi = num / den;
-    if (!literal) pi = (pi > 0.0f) ? pi : 0.0f;
+    const float pi_raw = num / den;
+    const float pi = (literal || pi_raw > 0.0f) ? pi_raw : 0.0f;
     pi_seg[seg] = pi;
+    if (diag) {   // clamped elements (raw pi negative or NaN) and elements
+        const double size = static_cast<double>(seg_off[seg + 1] - seg_off[seg]);
+        if (!(pi_raw >= 0.0f)) atomicAdd(&diag[2], size);
+        atomicAdd(&diag[3], size);
+    }
     // Recording: every element of the segment takes this factor, so its
     // histogram entry is one bin holding the segment's size.
     if (hist) {
@@ -831,27 +860,34 @@ hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, 
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream)
+template <bool DIAG>
+void launch_seg_step_d(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream)
 {
     const unsigned grid = blocks_for(a.Pp >> 2);
     switch (src) {
     case Source::Generated:
         if (bf16_out)
-            hipLaunchKernelGGL((seg_step_kernel<Source::Generated, true>), dim3(grid), dim3(kBlock),
-                               0, stream, a);
+            hipLaunchKernelGGL((seg_step_kernel<Source::Generated, true, DIAG>), dim3(grid),
+                               dim3(kBlock), 0, stream, a);
         else
-            hipLaunchKernelGGL((seg_step_kernel<Source::Generated, false>), dim3(grid), dim3(kBlock),
-                               0, stream, a);
+            hipLaunchKernelGGL((seg_step_kernel<Source::Generated, false, DIAG>), dim3(grid),
+                               dim3(kBlock), 0, stream, a);
         break;
     case Source::GivenF32:
-        hipLaunchKernelGGL((seg_step_kernel<Source::GivenF32, false>), dim3(grid), dim3(kBlock), 0,
-                           stream, a);
+        hipLaunchKernelGGL((seg_step_kernel<Source::GivenF32, false, DIAG>), dim3(grid),
+                           dim3(kBlock), 0, stream, a);
         break;
     case Source::GivenBF16:
-        hipLaunchKernelGGL((seg_step_kernel<Source::GivenBF16, false>), dim3(grid), dim3(kBlock), 0,
-                           stream, a);
+        hipLaunchKernelGGL((seg_step_kernel<Source::GivenBF16, false, DIAG>), dim3(grid),
+                           dim3(kBlock), 0, stream, a);
         break;
     }
+}
+
+hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream)
+{
+    if (a.diag) launch_seg_step_d<true>(a, src, bf16_out, stream);
+    else launch_seg_step_d<false>(a, src, bf16_out, stream);
     return hipGetLastError();
 }
 
@@ -870,11 +906,11 @@ hipError_t launch_seg_blocks(const double* part, int64_t npart, const int64_t* p
 hipError_t launch_seg_reduce(const double* sup, int64_t nsup, const int64_t* sup_off,
                              int32_t nseg, float* pi_seg, float k_eff, float eps, bool literal,
                              const int64_t* seg_off, uint32_t* hist, bool hist_per_seg,
-                             hipStream_t stream)
+                             double* diag, hipStream_t stream)
 {
     hipLaunchKernelGGL(seg_reduce_kernel, dim3(static_cast<unsigned>(nseg)), dim3(64), 0, stream,
                        sup, nsup, sup_off, pi_seg, k_eff, eps, literal ? 1 : 0, seg_off, hist,
-                       hist_per_seg ? 1 : 0);
+                       hist_per_seg ? 1 : 0, diag);
     return hipGetLastError();
 }
 

@@ -234,6 +234,39 @@ def test_pi_histograms(G, per_segment):
     assert np.array_equal(got, want if per_segment else want[:, 0])
 
 
+@pytest.mark.parametrize("mode", ["default", "pre_pull", "global_proxy", "kappa3_sqrt"])
+def test_diagnostics(G, mode):
+    """The energy sums (eqs. 11 and 22) and the clamp count under the segment
+    scope, against the oracle's per-commit diagnostics."""
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T = 9001, 4, 40
+    kw = {"default": {}, "pre_pull": dict(pull_mode=1), "global_proxy": dict(proxy_mode=1),
+          "kappa3_sqrt": dict(kappa=3.0, kappa_mode=1)}[mode]
+    hp = _hp(G, **kw)
+    seg = _partition("tensors", P)
+    h, ts = make_problem(P, 1e-3, 1.0, 5)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=5, pull_mode=hp.pull_mode)
+    with G.Gem(P, n, hp) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 9)
+        g.set_segments(seg)
+        G.gem_diag_enable(g.h, True)
+        g.sim_run(worker[:15], tau[:15], 8)
+        G.gem_diag_reset(g.h)
+        g.sim_run(worker[15:], tau[15:], 8)
+        d = G.gem_diag(g.h)
+        theta = g.theta()
+    st = O.State.initial(n, P)
+    _, _, dg = O.run_segments(_ohp(hp, 0.01, 0.1, 9), st, seg, worker, tau, h=h, ts=ts, diag=True)
+    later = dg[15:]
+    assert d.n_commits == T - 15
+    assert d.n_elem_commits == P * (T - 15)
+    assert d.n_clamped == int(later["n_clamped"].sum())
+    assert d.sum_ek == pytest.approx(float(later["sum_ek"].sum()), rel=1e-9)
+    assert d.sum_proxy == pytest.approx(float(later["sum_proxy"].sum()), rel=1e-9)
+    assert d.loss == pytest.approx(O.loss(st.theta, h, ts), rel=1e-10)
+    assert_parity("theta", theta, st.theta)
+
+
 def test_rejections(G):
     P, n = 1000, 2
     hp = _hp(G)
@@ -244,12 +277,8 @@ def test_rejections(G):
         for seg in ([0, 500], [1, P], [0, 500, 500, P], [0, 600, 400, P]):
             with pytest.raises(G.GemError):
                 g.set_segments(seg)
-        from paper_1805_08469_amd.workloads import make_problem
-        h, ts = make_problem(P, 1e-3, 1.0, 1)
-        g.set_quadratic(h, ts, 0.01, 0.1, 1)
-        G.gem_diag_enable(g.h, True)
         worker, tau = G.gem_schedule_make(n, 4, G.GEM_LAW_EXP, seed=1)
-        with pytest.raises(G.GemError):
+        with pytest.raises(G.GemError):      # no problem set
             g.sim_run(worker, tau, 4)
         assert g.clock == 0
 
