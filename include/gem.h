@@ -183,7 +183,8 @@ int gem_commit(gem_t* g, const float* dtheta_dev, int32_t worker_id);
  * each commit's tau (eq. 2) and must equal t_j - pull clock of its worker;
  * otherwise nothing is applied and ESTALE is returned.  Passes of up to
  * GEM_K_MAX commits stream theta once and each distinct worker's S and M rows
- * once. */
+ * once (under GEM_PI_SEGMENT each commit is applied on its own; see
+ * gem_set_segments). */
 int gem_commit_batch(gem_t* g, int32_t K, const void* const* dthetas_dev, int32_t dtype,
                      const int32_t* worker_ids, const int32_t* staleness);
 
@@ -209,7 +210,8 @@ int gem_schedule_make(int32_t n, int64_t T, const gem_schedule_law* law, uint64_
  * staleness tau[j] (host array, may be NULL, else checked like
  * gem_commit_batch), its update generated at the worker's snapshot (see
  * gem_sim_params), all fused into passes of at most K commits (1 <= K <=
- * GEM_K_MAX) that keep theta and the pass's (s, m) pairs in registers.  Needs
+ * GEM_K_MAX) that keep theta and the pass's (s, m) pairs in registers (under
+ * GEM_PI_SEGMENT K is checked but each commit is applied on its own).  Needs
  * gem_set_quadratic.  Errors: ESTATE, EINVAL, EWORKER, ESTALE. */
 int gem_sim_run(gem_t* g, const int32_t* worker, const int32_t* tau, int64_t T, int32_t K);
 
