@@ -138,8 +138,23 @@ def compare_rules(G, P: int = 1 << 20, T: int = 3000, every: int = 500, K: int =
                         curve.append(G.gem_diag(g.h).loss / P)
                 table.append({"lr": lr, "n": n, "rule": name, "commits_per_point": every,
                               "loss_per_param": curve})
+    # Appendix B: the high-energy proxy, kappa in both forms, 20 workers, eta = 0.01.
+    kappa_table = []
+    worker, tau = G.gem_schedule_make(20, T, G.GEM_LAW_EXP, seed=20)
+    for mode, name in ((G.GEM_KAPPA_LINEAR, "linear"), (G.GEM_KAPPA_SQRT, "sqrt")):
+        for kappa in (1.0, 2.0, 3.0, 4.0, 8.0):
+            hp = G.gem_hyperparams_default()
+            hp.kappa, hp.kappa_mode = kappa, mode
+            curve = []
+            with G.Gem(P, 20, hp) as g:
+                g.set_quadratic(h, ts, 0.01, 0.1, 9)
+                for c in range(0, T, every):
+                    g.sim_run(worker[c:c + every], tau[c:c + every], K)
+                    curve.append(G.gem_diag(g.h).loss / P)
+            kappa_table.append({"kappa": kappa, "form": name, "n": 20, "lr": 0.01,
+                                "commits_per_point": every, "loss_per_param": curve})
     return {"experiment": "rule comparison on a synthetic quadratic", "P": P, "T": T, "K": K,
-            "sigma": 0.1, "data": "synthetic", "table": table}
+            "sigma": 0.1, "data": "synthetic", "table": table, "kappa_table": kappa_table}
 
 
 def main() -> int:

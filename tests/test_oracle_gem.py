@@ -475,3 +475,40 @@ def test_pi_histograms_per_segment():
         _, _, sub = O.run(hp, P, O.State.initial(n, idx.size), idx, h[idx], ts[idx], w, tau,
                           pi_hist=True)
         assert np.array_equal(per[:, k], sub)
+
+
+def test_kappa_root_form_equals_linear_form_of_the_root():
+    """Appendix B's two forms of the high-energy proxy: sqrt(kappa)|m| with
+    kappa = 4 and 9 is the linear form with kappa = 2 and 3 (the roots are
+    exact in binary32), bit for bit, through the two code paths."""
+    P, n, T = 1500, 5, 300
+    h, ts = _quadratic(P, 41)
+    w, tau = O.schedule(n, T, O.LAW_EXP, 0, 0, seed=41)
+    for sq, lin in ((4.0, 2.0), (9.0, 3.0)):
+        a, b = O.State.initial(n, P), O.State.initial(n, P)
+        O.run(O.Hyper(lr=0.01, sigma=0.1, kappa=sq, kappa_mode=O.KAPPA_SQRT, seed=2), P, a,
+              np.arange(P), h, ts, w, tau)
+        O.run(O.Hyper(lr=0.01, sigma=0.1, kappa=lin, kappa_mode=O.KAPPA_LINEAR, seed=2), P, b,
+              np.arange(P), h, ts, w, tau)
+        for x, y in ((a.theta, b.theta), (a.S, b.S), (a.M, b.M)):
+            assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
+
+
+def test_higher_energy_proxy_speeds_progress_up_to_a_limit():
+    """Appendix B: raising kappa lets more of each update through and the loss
+    falls faster, up to a limit past which the run does worse.  Tiny problem,
+    20 workers: after 1000 commits the loss falls as kappa goes 1, 2, 3, 4;
+    after 3000, kappa = 8 ends above kappa = 2."""
+    P, n, T = 2048, 20, 3000
+    h, ts = _quadratic(P, 31)
+    w, tau = O.schedule(n, T, O.LAW_EXP, 0, 0, seed=n)
+    early, final = {}, {}
+    for kappa in (1.0, 2.0, 3.0, 4.0, 8.0):
+        hp = O.Hyper(lr=0.01, sigma=0.1, momentum=0.9, kappa=kappa, seed=9)
+        st = O.State.initial(n, P)
+        O.run(hp, P, st, np.arange(P), h, ts, w[:1000], tau[:1000])
+        early[kappa] = O.loss(st.theta, h, ts)
+        O.run(hp, P, st, np.arange(P), h, ts, w[1000:], tau[1000:])
+        final[kappa] = O.loss(st.theta, h, ts)
+    assert early[1.0] > early[2.0] > early[3.0] > early[4.0]
+    assert final[8.0] > final[2.0]
