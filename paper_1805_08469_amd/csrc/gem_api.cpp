@@ -26,8 +26,11 @@ struct gem_handle {
     gem_hyperparams hp{};
     hipStream_t stream = nullptr;
     float* theta = nullptr;   // [Pp]
-    float* S = nullptr;       // [n][Pp]
-    float* M = nullptr;       // [n][Pp]
+    // Snapshot and moment table (layout: gemk::tile_index); S is the
+    // allocation and addresses the snapshot pieces, M = S + kTileElems the
+    // moment pieces: S_w[i] = S[tile_index(n, w, i)], M_w[i] = M[tile_index(n, w, i)].
+    float* S = nullptr;
+    float* M = nullptr;
     float* h = nullptr;       // [Pp]
     float* ts = nullptr;      // [Pp]
     double* acc = nullptr;    // [5]: sum_ek, sum_proxy, n_clamped, n_elem_commits, loss
@@ -253,6 +256,7 @@ void base_args(const gem_handle* g, PassArgs& a)
     a.sink_mask = gemk::kSinkChunks - 1;
     a.Pp = g->Pp;
     a.P = g->P;
+    a.nw = g->n;
     a.key0 = static_cast<uint32_t>(g->sp.seed);
     a.key1 = static_cast<uint32_t>(g->sp.seed >> 32);
     a.neg_lr = -g->sp.lr;
@@ -428,6 +432,7 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
     a.npart = g->npart;
     a.Pp = g->Pp;
     a.P = g->P;
+    a.nw = g->n;
     a.pre_pull = g->hp.pull_mode == GEM_PULL_PRE_COMMIT;
     a.key0 = static_cast<uint32_t>(g->sp.seed);
     a.key1 = static_cast<uint32_t>(g->sp.seed >> 32);
@@ -530,7 +535,6 @@ int gem_destroy(gem_t* g)
     (void)hipStreamSynchronize(g->stream);
     (void)hipFree(g->theta);
     (void)hipFree(g->S);
-    (void)hipFree(g->M);
     (void)hipFree(g->h);
     (void)hipFree(g->ts);
     (void)hipFree(g->acc);
@@ -569,11 +573,11 @@ int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, ge
     // NULL is the device's null stream, which is also torch's default stream.
     g->stream = static_cast<hipStream_t>(stream);
     const size_t row = static_cast<size_t>(Pp) * sizeof(float);
-    const size_t tab = row * static_cast<size_t>(n);
+    const size_t tab = static_cast<size_t>(gemk::table_elems(n, Pp)) * sizeof(float);
     {
         hipError_t e = hipMalloc(&g->theta, row);
         if (e == hipSuccess) e = hipMalloc(&g->S, tab);
-        if (e == hipSuccess) e = hipMalloc(&g->M, tab);
+        if (e == hipSuccess) g->M = g->S + gemk::kTileElems;
         if (e == hipSuccess) e = hipMalloc(&g->acc, 8 * sizeof(double));
         if (e == hipSuccess) e = hipMalloc(&g->sink, 2 * gemk::kSinkChunks * 4 * sizeof(float));
         if (e != hipSuccess) {
@@ -585,8 +589,7 @@ int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, ge
     }
     const int rc = [&]() -> int {
         GEM_HIP(hipMemsetAsync(g->theta, 0, row, g->stream));
-        GEM_HIP(hipMemsetAsync(g->S, 0, tab, g->stream));
-        GEM_HIP(hipMemsetAsync(g->M, 0, tab, g->stream));
+        GEM_HIP(hipMemsetAsync(g->S, 0, tab, g->stream));   // every snapshot and moment
         GEM_HIP(hipMemsetAsync(g->acc, 0, 8 * sizeof(double), g->stream));
         GEM_HIP(hipMemsetAsync(g->sink, 0, 2 * gemk::kSinkChunks * 4 * sizeof(float), g->stream));
         GEM_HIP(hipStreamSynchronize(g->stream));
@@ -607,8 +610,8 @@ int gem_set_theta(gem_t* g, const float* theta0, int32_t in_is_device)
     GEM_HIP(hipMemcpyAsync(g->theta, theta0, bytes,
                            in_is_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
                            g->stream));
-    GEM_HIP(gemk::launch_fill_rows(g->S, g->theta, g->Pp, g->n, g->stream));
-    GEM_HIP(hipMemsetAsync(g->M, 0, static_cast<size_t>(g->Pp) * g->n * sizeof(float), g->stream));
+    GEM_HIP(gemk::launch_fill_rows(g->S, g->n, 0, g->n, g->Pp, g->theta, g->stream));
+    GEM_HIP(gemk::launch_fill_rows(g->M, g->n, 0, g->n, g->Pp, nullptr, g->stream));
     GEM_HIP(hipMemsetAsync(g->acc, 0, 8 * sizeof(double), g->stream));
     GEM_HIP(hipStreamSynchronize(g->stream));
     g->t = 0;
@@ -688,7 +691,7 @@ int gem_generate(gem_t* g, int32_t worker_id, void* out_dev, int32_t dtype)
     if (worker_id < 0 || worker_id >= g->n) return GEM_EWORKER;
     if (!aligned(out_dev, dtype == GEM_F32 ? 16 : 8)) return GEM_EALIGN;
     if (g->t > static_cast<int64_t>(UINT32_MAX)) return GEM_EINVAL;
-    GEM_HIP(gemk::launch_generate(g->S + static_cast<int64_t>(worker_id) * g->Pp, g->h, g->ts,
+    GEM_HIP(gemk::launch_generate(g->S, g->n, worker_id, g->h, g->ts,
                                   out_dev, dtype == GEM_BF16, g->P, static_cast<uint32_t>(g->t),
                                   static_cast<uint32_t>(g->sp.seed),
                                   static_cast<uint32_t>(g->sp.seed >> 32), -g->sp.lr, g->sp.sigma,
@@ -726,12 +729,28 @@ int gem_read_state(gem_t* g, int32_t w, int32_t which, float* out, int32_t out_i
     if (!g || !out) return GEM_EINVAL;
     if (w < 0 || w >= g->n) return GEM_EWORKER;
     if (which != GEM_SNAPSHOT && which != GEM_MOMENT) return GEM_EINVAL;
-    const float* src = (which == GEM_SNAPSHOT ? g->S : g->M) + static_cast<int64_t>(w) * g->Pp;
-    GEM_HIP(hipMemcpyAsync(out, src, static_cast<size_t>(g->P) * sizeof(float),
-                           out_is_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost,
-                           g->stream));
-    GEM_HIP(hipStreamSynchronize(g->stream));
-    return GEM_OK;
+    const float* base = which == GEM_SNAPSHOT ? g->S : g->M;
+    if (out_is_device) {
+        GEM_HIP(gemk::launch_read_row(base, g->n, w, g->P, out, g->stream));
+        GEM_HIP(hipStreamSynchronize(g->stream));
+        return GEM_OK;
+    }
+    // The row is spread over the table's tiles: gather it into a device
+    // staging row, then copy that to the host.
+    float* stage = nullptr;
+    if (hipMalloc(&stage, static_cast<size_t>(g->P) * sizeof(float)) != hipSuccess) {
+        (void)hipGetLastError();
+        return GEM_ENOMEM;
+    }
+    int rc = GEM_OK;
+    if (gemk::launch_read_row(base, g->n, w, g->P, stage, g->stream) != hipSuccess ||
+        hipMemcpyAsync(out, stage, static_cast<size_t>(g->P) * sizeof(float), hipMemcpyDeviceToHost,
+                       g->stream) != hipSuccess ||
+        hipStreamSynchronize(g->stream) != hipSuccess)
+        rc = GEM_EHIP;
+    (void)hipStreamSynchronize(g->stream);
+    (void)hipFree(stage);
+    return rc;
 }
 
 int gem_gather(gem_t* g, const int64_t* idx, int64_t count, float* theta_out, float* S_out,
@@ -758,15 +777,16 @@ int gem_gather(gem_t* g, const int64_t* idx, int64_t count, float* theta_out, fl
             rc = GEM_EHIP;
             break;
         }
-        for (int32_t w = 0; w < g->n && rc == GEM_OK; ++w) {
-            if (S_out && gemk::launch_gather(g->S + static_cast<int64_t>(w) * g->Pp, d_idx, count,
-                                             d_out + (1 + w) * count, g->stream) != hipSuccess)
-                rc = GEM_EHIP;
-            if (M_out && gemk::launch_gather(g->M + static_cast<int64_t>(w) * g->Pp, d_idx, count,
-                                             d_out + (1 + g->n + w) * count, g->stream) != hipSuccess)
-                rc = GEM_EHIP;
+        if (S_out && gemk::launch_gather_rows(g->S, g->n, d_idx, count, d_out + count,
+                                              g->stream) != hipSuccess) {
+            rc = GEM_EHIP;
+            break;
         }
-        if (rc) break;
+        if (M_out && gemk::launch_gather_rows(g->M, g->n, d_idx, count, d_out + (1 + g->n) * count,
+                                              g->stream) != hipSuccess) {
+            rc = GEM_EHIP;
+            break;
+        }
         std::vector<float> host(static_cast<size_t>(count * rows));
         if (hipMemcpyAsync(host.data(), d_out, host.size() * sizeof(float), hipMemcpyDeviceToHost,
                            g->stream) != hipSuccess ||
@@ -801,11 +821,9 @@ int gem_reset_worker(gem_t* g, int32_t w)
 {
     if (!g) return GEM_EINVAL;
     if (w < 0 || w >= g->n) return GEM_EWORKER;
-    const size_t row = static_cast<size_t>(g->Pp) * sizeof(float);
-    GEM_HIP(hipMemcpyAsync(g->S + static_cast<int64_t>(w) * g->Pp, g->theta, row,
-                           hipMemcpyDeviceToDevice, g->stream));
+    GEM_HIP(gemk::launch_fill_rows(g->S, g->n, w, 1, g->Pp, g->theta, g->stream));
     if (g->hp.proxy_mode == GEM_PROXY_LOCAL)
-        GEM_HIP(hipMemsetAsync(g->M + static_cast<int64_t>(w) * g->Pp, 0, row, g->stream));
+        GEM_HIP(gemk::launch_fill_rows(g->M, g->n, w, 1, g->Pp, nullptr, g->stream));
     g->pc[w] = g->t;
     return GEM_OK;
 }
@@ -1063,14 +1081,68 @@ int read_rows(gem_handle* g, FILE* f, float* dev, int64_t rows, std::vector<floa
     return GEM_OK;
 }
 
+// Rows of the table pieces at base (g->S or g->M), one worker after another,
+// through a device staging row of Pp elements.
+int write_table(gem_handle* g, FILE* f, const float* base, float* stage, std::vector<float>& buf)
+{
+    for (int32_t w = 0; w < g->n; ++w) {
+        GEM_HIP(gemk::launch_read_row(base, g->n, w, g->P, stage, g->stream));
+        GEM_HIP(hipMemcpyAsync(buf.data(), stage, static_cast<size_t>(g->P) * sizeof(float),
+                               hipMemcpyDeviceToHost, g->stream));
+        GEM_HIP(hipStreamSynchronize(g->stream));
+        if (std::fwrite(buf.data(), sizeof(float), static_cast<size_t>(g->P), f) !=
+            static_cast<size_t>(g->P))
+            return GEM_EIO;
+    }
+    return GEM_OK;
+}
+
+// The staging row's padding [P, Pp) is zero, so each row's padding stays zero.
+int read_table(gem_handle* g, FILE* f, float* base, float* stage, std::vector<float>& buf)
+{
+    for (int32_t w = 0; w < g->n; ++w) {
+        if (std::fread(buf.data(), sizeof(float), static_cast<size_t>(g->P), f) !=
+            static_cast<size_t>(g->P))
+            return GEM_EIO;
+        GEM_HIP(hipMemcpyAsync(stage, buf.data(), static_cast<size_t>(g->P) * sizeof(float),
+                               hipMemcpyHostToDevice, g->stream));
+        GEM_HIP(gemk::launch_fill_rows(base, g->n, w, 1, g->Pp, stage, g->stream));
+        GEM_HIP(hipStreamSynchronize(g->stream));
+    }
+    return GEM_OK;
+}
+
+// A zeroed device row of Pp elements for checkpoint I/O, or null.
+float* staging_row(gem_handle* g)
+{
+    float* stage = nullptr;
+    const size_t bytes = static_cast<size_t>(g->Pp) * sizeof(float);
+    if (hipMalloc(&stage, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    if (hipMemsetAsync(stage, 0, bytes, g->stream) != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipFree(stage);
+        return nullptr;
+    }
+    return stage;
+}
+
 }  // namespace
 
 int gem_save(gem_t* g, const char* path)
 {
     if (!g || !path) return GEM_EINVAL;
     GEM_HIP(hipStreamSynchronize(g->stream));
+    float* stage = staging_row(g);
+    if (!stage) return GEM_ENOMEM;
     FILE* f = std::fopen(path, "wb");
-    if (!f) return GEM_EIO;
+    if (!f) {
+        (void)hipStreamSynchronize(g->stream);
+        (void)hipFree(stage);
+        return GEM_EIO;
+    }
     CkptHeader hd;
     std::memset(&hd, 0, sizeof(hd));
     std::memcpy(hd.magic, kCkptMagic, 8);
@@ -1084,8 +1156,8 @@ int gem_save(gem_t* g, const char* path)
     std::vector<float> buf(static_cast<size_t>(g->P));
     int rc = std::fwrite(&hd, sizeof(hd), 1, f) == 1 ? GEM_OK : GEM_EIO;
     if (!rc) rc = write_rows(g, f, g->theta, 1, buf);
-    if (!rc) rc = write_rows(g, f, g->S, g->n, buf);
-    if (!rc) rc = write_rows(g, f, g->M, g->n, buf);
+    if (!rc) rc = write_table(g, f, g->S, stage, buf);
+    if (!rc) rc = write_table(g, f, g->M, stage, buf);
     if (!rc && std::fwrite(g->pc.data(), sizeof(int64_t), g->pc.size(), f) != g->pc.size()) rc = GEM_EIO;
     if (!rc && g->have_problem) rc = write_rows(g, f, g->h, 1, buf);
     if (!rc && g->have_problem) rc = write_rows(g, f, g->ts, 1, buf);
@@ -1093,6 +1165,8 @@ int gem_save(gem_t* g, const char* path)
         std::fwrite(g->seg_host.data(), sizeof(int64_t), g->seg_host.size(), f) != g->seg_host.size())
         rc = GEM_EIO;
     if (std::fclose(f) != 0 && !rc) rc = GEM_EIO;
+    (void)hipStreamSynchronize(g->stream);
+    (void)hipFree(stage);
     return rc;
 }
 
@@ -1126,6 +1200,11 @@ int gem_load(gem_t* g, const char* path)
         }
         if (!rc && std::fseek(f, static_cast<long>(sizeof(hd)), SEEK_SET) != 0) rc = GEM_EIO;
     }
+    float* stage = nullptr;
+    if (!rc) {
+        stage = staging_row(g);
+        if (!stage) rc = GEM_ENOMEM;
+    }
     if (!rc && g->hist_on && g->hist_seg)
         g->hist_on = false;   // the partition under a per-segment recording may change
     if (!rc && !seg.empty()) rc = build_segments(g, seg);
@@ -1142,12 +1221,14 @@ int gem_load(gem_t* g, const char* path)
     std::vector<float> buf(static_cast<size_t>(g->P));
     std::vector<int64_t> pc(static_cast<size_t>(g->n));
     if (!rc) rc = read_rows(g, f, g->theta, 1, buf);
-    if (!rc) rc = read_rows(g, f, g->S, g->n, buf);
-    if (!rc) rc = read_rows(g, f, g->M, g->n, buf);
+    if (!rc) rc = read_table(g, f, g->S, stage, buf);
+    if (!rc) rc = read_table(g, f, g->M, stage, buf);
     if (!rc && std::fread(pc.data(), sizeof(int64_t), pc.size(), f) != pc.size()) rc = GEM_EIO;
     if (!rc && hd.have_problem) rc = read_rows(g, f, g->h, 1, buf);
     if (!rc && hd.have_problem) rc = read_rows(g, f, g->ts, 1, buf);
     std::fclose(f);
+    (void)hipStreamSynchronize(g->stream);
+    (void)hipFree(stage);
     if (rc) return rc;
     if (seg.empty() && !g->seg_host.empty()) {
         GEM_HIP(hipStreamSynchronize(g->stream));

@@ -289,13 +289,13 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
         // to the sink.
         const int64_t sink_off = (ch.c & a.sink_mask) * 4;
         const bool st = dst == kToMemory;
-        const int64_t so = st ? static_cast<int64_t>(w) * a.Pp + ch.off : sink_off;
+        const int64_t so = st ? tile_index(a.nw, w, ch.off) : sink_off;
         const bool st_m = st && !global_m;
         *reinterpret_cast<float4*>((st ? a.S : a.sink_S) + so) = r.out.s;
         *reinterpret_cast<float4*>((st_m ? a.M : a.sink_M) + (st_m ? so : sink_off)) = r.out.m;
         const bool pf = (route & kRoutePrefetch) != 0;
         const int jn = j + kPrefetchDepth < a.K ? j + kPrefetchDepth : j;
-        const int64_t lo = pf ? static_cast<int64_t>(a.worker[jn]) * a.Pp + ch.off : sink_off;
+        const int64_t lo = pf ? tile_index(a.nw, a.worker[jn], ch.off) : sink_off;
         const bool pf_m = pf && !global_m;
         r.next.s = *reinterpret_cast<const float4*>((pf ? a.S : a.sink_S) + lo);
         r.next.m = *reinterpret_cast<const float4*>((pf_m ? a.M : a.sink_M) + (pf_m ? lo : sink_off));
@@ -325,7 +325,9 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     ch.mg = ch.th;
     const bool global_m = V == Variant::FastGlobal ||
                           (V == Variant::General && (a.mode & kModeGlobalProxy));
-    if (global_m && ch.active) ch.mg = *reinterpret_cast<const float4*>(a.M + ch.off);
+    // The shared moment is worker 0's.
+    const int64_t mg_at = tile_index(a.nw, 0, ch.off);
+    if (global_m && ch.active) ch.mg = *reinterpret_cast<const float4*>(a.M + mg_at);
     const int K = a.K;
     // Ring of prefetched rows, unrolled kPrefetchDepth ways so that every entry
     // is a fixed set of registers: commit j reads ring[j mod depth] and refills
@@ -346,7 +348,7 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
             // With the shared moment only the snapshot row is read.
             const bool mem = u < K && (a.routes[u] & kRouteSlotMask) == kFromRing;
             const bool mem_m = mem && !global_m;
-            const int64_t lo = mem ? static_cast<int64_t>(a.worker[u]) * a.Pp + ch.off : sink_off;
+            const int64_t lo = mem ? tile_index(a.nw, a.worker[u], ch.off) : sink_off;
             ring[u].s = *reinterpret_cast<const float4*>((mem ? a.S : a.sink_S) + lo);
             ring[u].m = *reinterpret_cast<const float4*>((mem_m ? a.M : a.sink_M) +
                                                          (mem_m ? lo : sink_off));
@@ -401,7 +403,7 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
         }
     }
     if (ch.active) *reinterpret_cast<float4*>(a.theta + ch.off) = ch.th;
-    if (global_m && ch.active) *reinterpret_cast<float4*>(a.M + ch.off) = ch.mg;
+    if (global_m && ch.active) *reinterpret_cast<float4*>(a.M + mg_at) = ch.mg;
 
     if (DIAG && a.diag) {
         __shared__ double red[4][kBlock];
@@ -483,7 +485,7 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
         // The pending commit's update: the caller's, or generated again at
         // the worker's snapshot, which its pull below replaces.
         float4 d;
-        float* srow = a.S + static_cast<int64_t>(a.w_prev) * a.Pp + off;
+        float* srow = a.S + tile_index(a.nw, a.w_prev, off);
         float4 sp = make_float4(0.f, 0.f, 0.f, 0.f);
         if (SRC == Source::Generated || DIAG) sp = f4(srow);
         if (SRC == Source::Generated) {
@@ -509,7 +511,7 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
         if (DIAG) {
             // E_k against the worker's snapshot (eq. 11) and the proxy energy
             // (eq. 22) of the pending commit, whose moment is already stored.
-            const float4 mp = f4(a.M + static_cast<int64_t>(a.m_row_prev) * a.Pp + off);
+            const float4 mp = f4(a.M + tile_index(a.nw, a.m_row_prev, off));
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 if (off + k < a.P) {
@@ -540,7 +542,7 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
     d = mo;
     if (active) {
         if (a.apply && a.w_cur == a.w_prev) s = pick(a.pre_pull, th_old, th);   // just pulled
-        else s = f4(a.S + static_cast<int64_t>(a.w_cur) * a.Pp + off);
+        else s = f4(a.S + tile_index(a.nw, a.w_cur, off));
         if (SRC == Source::Generated) {
             const float4 z = normals4(static_cast<uint64_t>(c), a.t, a.key0, a.key1);
             d.x = stale_update<BF16>(a.neg_lr, a.sigma, s.x, hv.x, tv.x, z.x);
@@ -550,7 +552,7 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
         } else {
             d = load_given<SRC>(a.upd_cur, c, a.P);
         }
-        float* mrow = a.M + static_cast<int64_t>(a.m_row) * a.Pp + off;
+        float* mrow = a.M + tile_index(a.nw, a.m_row, off);
         mo = f4(mrow);
         float4 m;
         m.x = __builtin_fmaf(a.mu, mo.x, d.x);     // Alg. 1: m <- mu m + dtheta
@@ -705,8 +707,8 @@ __global__ __launch_bounds__(64) void seg_reduce_kernel(const double* __restrict
 }
 
 template <bool BF16>
-__global__ __launch_bounds__(kBlock) void generate_kernel(const float* __restrict__ S_w,
-                                                         const float* __restrict__ h,
+__global__ __launch_bounds__(kBlock) void generate_kernel(const float* __restrict__ S, int64_t nw,
+                                                         int32_t w, const float* __restrict__ h,
                                                          const float* __restrict__ ts, void* out,
                                                          int64_t P, uint32_t t, uint32_t key0,
                                                          uint32_t key1, float neg_lr, float sigma)
@@ -714,7 +716,7 @@ __global__ __launch_bounds__(kBlock) void generate_kernel(const float* __restric
     const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const int64_t i0 = c * 4;
     if (i0 >= P) return;
-    const float4 s = *reinterpret_cast<const float4*>(S_w + i0);
+    const float4 s = *reinterpret_cast<const float4*>(S + tile_index(nw, w, i0));
     const float4 hv = *reinterpret_cast<const float4*>(h + i0);
     const float4 tv = *reinterpret_cast<const float4*>(ts + i0);
     const float4 z = normals4(static_cast<uint64_t>(c), t, key0, key1);
@@ -745,14 +747,28 @@ __global__ __launch_bounds__(kBlock) void generate_kernel(const float* __restric
     }
 }
 
-__global__ __launch_bounds__(kBlock) void fill_rows_kernel(float* dst, const float* row, int64_t Pp,
-                                                           int32_t rows)
+// Rows w0 .. w0 + rows - 1 of the table pieces at base, over [0, Pp): set to
+// row (16-byte aligned), or to zero when row is null.
+__global__ __launch_bounds__(kBlock) void fill_rows_kernel(float* base, int64_t nw, int32_t w0,
+                                                           int32_t rows, int64_t Pp,
+                                                           const float* row)
 {
     const int64_t nchunk = Pp >> 2;
     const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     if (c >= nchunk) return;
-    const float4 v = reinterpret_cast<const float4*>(row)[c];
-    for (int32_t r = 0; r < rows; ++r) reinterpret_cast<float4*>(dst + static_cast<int64_t>(r) * Pp)[c] = v;
+    const float4 v = row ? reinterpret_cast<const float4*>(row)[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int32_t r = 0; r < rows; ++r)
+        *reinterpret_cast<float4*>(base + tile_index(nw, w0 + r, c * 4)) = v;
+}
+
+// out[i] = worker w's element i of the table pieces at base, i < P (out of
+// any alignment).
+__global__ __launch_bounds__(kBlock) void read_row_kernel(const float* __restrict__ base,
+                                                          int64_t nw, int32_t w, int64_t P,
+                                                          float* __restrict__ out)
+{
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (i < P) out[i] = base[tile_index(nw, w, i)];
 }
 
 __global__ __launch_bounds__(kBlock) void gather_kernel(const float* __restrict__ src,
@@ -761,6 +777,18 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(const float* __restrict_
 {
     const int64_t k = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     if (k < count) out[k] = src[idx[k]];
+}
+
+// out[w * count + k] = worker w's element idx[k] of the table pieces at base,
+// for workers w = w0 + blockIdx.y.
+__global__ __launch_bounds__(kBlock) void gather_rows_kernel(const float* __restrict__ base,
+                                                             int64_t nw, int64_t w0,
+                                                             const int64_t* __restrict__ idx,
+                                                             int64_t count, float* __restrict__ out)
+{
+    const int64_t k = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const int64_t w = w0 + blockIdx.y;
+    if (k < count) out[w * count + k] = base[tile_index(nw, w, idx[k])];
 }
 
 __global__ __launch_bounds__(kBlock) void loss_kernel(const float* __restrict__ theta,
@@ -784,33 +812,19 @@ __global__ __launch_bounds__(kBlock) void loss_kernel(const float* __restrict__ 
     if (threadIdx.x == 0) atomicAdd(out, red[0]);
 }
 
-// Plain copy, the bandwidth reference: each block moves tiles of
-// kCopyUnroll * kBlock 16-byte chunks, all loads of a tile before its stores.
-constexpr int kCopyUnroll = 4;
-
+// Plain copy, the bandwidth reference: one 16-byte chunk per thread and
+// trip of a grid-stride loop whose grid covers the whole copy up to 4 GiB
+// (2^20 blocks).  On MI355X this moves 6.3 TB/s of reads plus writes; tiles
+// of four chunks per thread reach 5.6 TB/s.
 __global__ __launch_bounds__(kBlock) void copy_kernel(const float* __restrict__ src,
                                                       float* __restrict__ dst, int64_t count)
 {
     const int64_t n4 = count / 4;
     const float4* s4 = reinterpret_cast<const float4*>(src);
     float4* d4 = reinterpret_cast<float4*>(dst);
-    const int64_t tile = static_cast<int64_t>(kCopyUnroll) * kBlock;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * tile;
-    for (int64_t base = static_cast<int64_t>(blockIdx.x) * tile + threadIdx.x; base < n4;
-         base += stride) {
-        float4 v[kCopyUnroll];
-#pragma unroll
-        for (int u = 0; u < kCopyUnroll; ++u) {
-            const int64_t k = base + static_cast<int64_t>(u) * kBlock;
-            v[u] = k < n4 ? s4[k] : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-#pragma unroll
-        for (int u = 0; u < kCopyUnroll; ++u) {
-            const int64_t k = base + static_cast<int64_t>(u) * kBlock;
-            if (k < n4) d4[k] = v[u];
-        }
-    }
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
     const int64_t first = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    for (int64_t k = first; k < n4; k += stride) d4[k] = s4[k];
     if (first < count - n4 * 4) dst[n4 * 4 + first] = src[n4 * 4 + first];
 }
 
@@ -914,24 +928,36 @@ hipError_t launch_seg_reduce(const double* sup, int64_t nsup, const int64_t* sup
     return hipGetLastError();
 }
 
-hipError_t launch_generate(const float* S_w, const float* h, const float* ts, void* out, bool bf16,
-                           int64_t P, uint32_t t, uint32_t key0, uint32_t key1, float neg_lr,
-                           float sigma, hipStream_t stream)
+hipError_t launch_generate(const float* S, int64_t nw, int32_t w, const float* h,
+                           const float* ts, void* out, bool bf16, int64_t P, uint32_t t,
+                           uint32_t key0, uint32_t key1, float neg_lr, float sigma,
+                           hipStream_t stream)
 {
     const unsigned grid = blocks_for((P + 3) / 4);
     if (bf16)
-        hipLaunchKernelGGL(generate_kernel<true>, dim3(grid), dim3(kBlock), 0, stream, S_w, h, ts,
-                           out, P, t, key0, key1, neg_lr, sigma);
+        hipLaunchKernelGGL(generate_kernel<true>, dim3(grid), dim3(kBlock), 0, stream, S, nw, w, h,
+                           ts, out, P, t, key0, key1, neg_lr, sigma);
     else
-        hipLaunchKernelGGL(generate_kernel<false>, dim3(grid), dim3(kBlock), 0, stream, S_w, h, ts,
-                           out, P, t, key0, key1, neg_lr, sigma);
+        hipLaunchKernelGGL(generate_kernel<false>, dim3(grid), dim3(kBlock), 0, stream, S, nw, w, h,
+                           ts, out, P, t, key0, key1, neg_lr, sigma);
     return hipGetLastError();
 }
 
-hipError_t launch_fill_rows(float* dst, const float* row, int64_t Pp, int32_t rows, hipStream_t stream)
+hipError_t launch_fill_rows(float* base, int64_t nw, int32_t w0, int32_t rows, int64_t Pp,
+                            const float* row, hipStream_t stream)
 {
-    hipLaunchKernelGGL(fill_rows_kernel, dim3(blocks_for(Pp >> 2)), dim3(kBlock), 0, stream, dst,
-                       row, Pp, rows);
+    if (rows <= 0 || Pp <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_rows_kernel, dim3(blocks_for(Pp >> 2)), dim3(kBlock), 0, stream, base,
+                       nw, w0, rows, Pp, row);
+    return hipGetLastError();
+}
+
+hipError_t launch_read_row(const float* base, int64_t nw, int32_t w, int64_t P, float* out,
+                           hipStream_t stream)
+{
+    if (P <= 0) return hipSuccess;
+    hipLaunchKernelGGL(read_row_kernel, dim3(blocks_for(P)), dim3(kBlock), 0, stream, base, nw, w,
+                       P, out);
     return hipGetLastError();
 }
 
@@ -942,6 +968,21 @@ hipError_t launch_gather(const float* src, const int64_t* idx, int64_t count, fl
     hipLaunchKernelGGL(gather_kernel, dim3(blocks_for(count)), dim3(kBlock), 0, stream, src, idx,
                        count, out);
     return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const float* base, int64_t nw, const int64_t* idx, int64_t count,
+                              float* out, hipStream_t stream)
+{
+    if (count <= 0 || nw <= 0) return hipSuccess;
+    constexpr int64_t kMaxY = 65535;   // grid y limit
+    for (int64_t w0 = 0; w0 < nw; w0 += kMaxY) {
+        const int64_t rows = nw - w0 < kMaxY ? nw - w0 : kMaxY;
+        hipLaunchKernelGGL(gather_rows_kernel, dim3(blocks_for(count), static_cast<unsigned>(rows)),
+                           dim3(kBlock), 0, stream, base, nw, w0, idx, count, out);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_loss(const float* theta, const float* h, const float* ts, int64_t P, double* out,
@@ -956,9 +997,9 @@ hipError_t launch_loss(const float* theta, const float* h, const float* ts, int6
 hipError_t launch_copy(const float* src, float* dst, int64_t count, hipStream_t stream)
 {
     if (count <= 0) return hipSuccess;
-    const int64_t tile = static_cast<int64_t>(kCopyUnroll) * kBlock;
-    const int64_t want = (count / 4 + tile - 1) / tile;
-    const unsigned grid = static_cast<unsigned>(want < 1 ? 1 : want < 131072 ? want : 131072);
+    const int64_t want = (count / 4 + kBlock - 1) / kBlock;
+    const int64_t cap = int64_t{1} << 20;
+    const unsigned grid = static_cast<unsigned>(want < 1 ? 1 : want < cap ? want : cap);
     hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(kBlock), 0, stream, src, dst, count);
     return hipGetLastError();
 }

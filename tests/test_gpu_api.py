@@ -174,8 +174,9 @@ def test_empty_batch_and_run_are_no_ops(env):
 
 def test_copy_probe(env):
     torch, G = env
-    # the last count needs more tiles than the grid holds (grid-stride loop)
-    for count in (1, 4, 1003, 1 << 20, (131072 * 1024 + 5) * 4 + 3):
+    # the last count needs more chunks than the grid's 2^20 blocks of 256
+    # threads hold (grid-stride loop), with a ragged tail
+    for count in (1, 4, 1003, 1 << 20, ((1 << 28) + 5) * 4 + 3):
         src = torch.arange(count, dtype=torch.float32, device="cuda")
         dst = torch.zeros(count, device="cuda")
         assert G.gem_copy_f32(src.data_ptr(), dst.data_ptr(), count) == G.GEM_OK
