@@ -77,7 +77,8 @@ typedef struct gem_handle gem_t;
  * Sec. 4: DOWNPOUR (commit dtheta unchanged, eq. 1) and adaptive staleness
  * (commit dtheta / (tau + 1)).  proxy_mode LOCAL keeps one first moment per
  * worker (Sec. 3.3); GLOBAL keeps one moment shared by all workers, refreshed
- * by every commit (the global proxy of Sec. 6), stored as row 0 of M.
+ * by every commit (the global proxy of Sec. 6), stored as worker 0's moment
+ * (gem_read_state(g, 0, GEM_MOMENT, ...) returns it).
  * pi_scope ELEMENT computes pi per parameter from absolute values (eq. 18);
  * SEGMENT computes one pi per segment of the parameter vector from Euclidean
  * norms over the segment (see gem_set_segments; GEM rule only). */
@@ -218,7 +219,10 @@ int gem_sim_run(gem_t* g, const int32_t* worker, const int32_t* tau, int64_t T, 
 /* Copy theta (P floats) to out (host, or device if out_is_device). */
 int gem_read_theta(gem_t* g, float* out, int32_t out_is_device);
 
-/* Copy worker w's snapshot (which = GEM_SNAPSHOT) or moment (GEM_MOMENT) row. */
+/* Copy worker w's snapshot (which = GEM_SNAPSHOT) or moment (GEM_MOMENT) row,
+ * P elements, to out (device memory of any alignment if out_is_device, else
+ * host memory); synchronises.  A host copy goes through a temporary device row
+ * of P elements: GEM_ENOMEM if it cannot be allocated. */
 int gem_read_state(gem_t* g, int32_t w, int32_t which, float* out, int32_t out_is_device);
 
 /* Gather theta[idx[k]] into theta_out[k] and S[w][idx[k]], M[w][idx[k]] into
@@ -313,7 +317,9 @@ int gem_stats_reset(gem_t* g);
  * Load requires a handle of the same P and n, and checks the whole file
  * (size, partition) before it changes any state.  Resume is bit-exact: noise
  * is a function of (seed, t, i).  GEM_EIO for an unreadable, foreign or
- * truncated file. */
+ * truncated file; GEM_ENOMEM (before any file or state is touched) when the
+ * device row of P' elements that stages S and M cannot be allocated.  The file
+ * holds each row as P contiguous floats, whatever the device layout. */
 int gem_save(gem_t* g, const char* path);
 int gem_load(gem_t* g, const char* path);
 
