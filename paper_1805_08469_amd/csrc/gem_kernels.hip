@@ -164,6 +164,7 @@ struct Rows {
 struct Chunk {
     int64_t c;       // chunk index (= Philox counter q of its four elements)
     int64_t off;     // element offset 4c
+    int64_t tb;      // table index of worker 0's snapshot chunk; worker w's is tb + w * 2 * kTileElems
     bool active;
     bool l0, l1, l2, l3;   // elements below the true length (diagnostics)
     int32_t sg[4];         // per-segment histograms: each element's segment
@@ -289,13 +290,14 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
         // to the sink.
         const int64_t sink_off = (ch.c & a.sink_mask) * 4;
         const bool st = dst == kToMemory;
-        const int64_t so = st ? tile_index(a.nw, w, ch.off) : sink_off;
+        const int64_t so = st ? ch.tb + (static_cast<int64_t>(w) << (kTileShift + 1)) : sink_off;
         const bool st_m = st && !global_m;
         *reinterpret_cast<float4*>((st ? a.S : a.sink_S) + so) = r.out.s;
         *reinterpret_cast<float4*>((st_m ? a.M : a.sink_M) + (st_m ? so : sink_off)) = r.out.m;
         const bool pf = (route & kRoutePrefetch) != 0;
         const int jn = j + kPrefetchDepth < a.K ? j + kPrefetchDepth : j;
-        const int64_t lo = pf ? tile_index(a.nw, a.worker[jn], ch.off) : sink_off;
+        const int64_t lo =
+            pf ? ch.tb + (static_cast<int64_t>(a.worker[jn]) << (kTileShift + 1)) : sink_off;
         const bool pf_m = pf && !global_m;
         r.next.s = *reinterpret_cast<const float4*>((pf ? a.S : a.sink_S) + lo);
         r.next.m = *reinterpret_cast<const float4*>((pf_m ? a.M : a.sink_M) + (pf_m ? lo : sink_off));
@@ -325,9 +327,9 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     ch.mg = ch.th;
     const bool global_m = V == Variant::FastGlobal ||
                           (V == Variant::General && (a.mode & kModeGlobalProxy));
+    ch.tb = tile_index(a.nw, 0, ch.off);
     // The shared moment is worker 0's.
-    const int64_t mg_at = tile_index(a.nw, 0, ch.off);
-    if (global_m && ch.active) ch.mg = *reinterpret_cast<const float4*>(a.M + mg_at);
+    if (global_m && ch.active) ch.mg = *reinterpret_cast<const float4*>(a.M + ch.tb);
     const int K = a.K;
     // Ring of prefetched rows, unrolled kPrefetchDepth ways so that every entry
     // is a fixed set of registers: commit j reads ring[j mod depth] and refills
@@ -348,7 +350,8 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
             // With the shared moment only the snapshot row is read.
             const bool mem = u < K && (a.routes[u] & kRouteSlotMask) == kFromRing;
             const bool mem_m = mem && !global_m;
-            const int64_t lo = mem ? tile_index(a.nw, a.worker[u], ch.off) : sink_off;
+            const int64_t lo =
+                mem ? ch.tb + (static_cast<int64_t>(a.worker[u]) << (kTileShift + 1)) : sink_off;
             ring[u].s = *reinterpret_cast<const float4*>((mem ? a.S : a.sink_S) + lo);
             ring[u].m = *reinterpret_cast<const float4*>((mem_m ? a.M : a.sink_M) +
                                                          (mem_m ? lo : sink_off));
@@ -403,7 +406,7 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
         }
     }
     if (ch.active) *reinterpret_cast<float4*>(a.theta + ch.off) = ch.th;
-    if (global_m && ch.active) *reinterpret_cast<float4*>(a.M + mg_at) = ch.mg;
+    if (global_m && ch.active) *reinterpret_cast<float4*>(a.M + ch.tb) = ch.mg;
 
     if (DIAG && a.diag) {
         __shared__ double red[4][kBlock];
