@@ -222,6 +222,9 @@ def main() -> int:
     hp.pi_scope = G.GEM_PI_SEGMENT if args.pi_scope == "segment" else G.GEM_PI_ELEMENT
     fast = (args.rule, args.pi, args.kappa, args.pi_scope) == ("gem", "clamp0", 1.0, "element")
     variant = "General" if not fast else "FastGlobal" if args.proxy == "global" else "Fast"
+    # The library's ring depth for these passes (deep: the default rule with
+    # per-worker moments in passes of at least 16 commits).
+    depth = 4 if variant == "Fast" and wl.K >= 16 else 2
 
     stream = torch.cuda.current_stream()
     g = G.Gem(wl.P, wl.n, hp, stream=stream.cuda_stream)
@@ -298,7 +301,7 @@ def main() -> int:
             "alg_bytes_per_launch": alg_per_pass,
             "avg_launch_ms": avg_pass_s * 1e3,
             "kernel": ("seg_step_kernel + seg_reduce_kernel" if args.pi_scope == "segment"
-                       else "pass_kernel<Generated, %s>" % variant),
+                       else "pass_kernel<Generated, %s, depth %d>" % (variant, depth)),
             "copy_ceiling_GBps": copy_gbs,
             "frac_of_copy": achieved / copy_gbs,
         },

@@ -160,16 +160,20 @@ struct Pass {
     int32_t row_writes = 0;   // and writes
 };
 
-// Routes of one pass of k commits (see gem_internal.hpp).  A worker's chunk
-// is read from memory at its first commit in the pass and written back at its
-// last; in between it waits in one of kHeldSlots register slots.  When no slot
-// is free the chunk is written back and re-read, which is only valid if the
-// re-read is at least kPrefetchDepth commits later: the prefetch for commit
-// j + depth is issued right after commit j's store.  If a nearer repeat finds
-// no free slot the pass has to end after commit j: the function then returns
+// Routes of one pass of k commits for a kernel whose ring prefetches depth
+// commits ahead (see gem_internal.hpp).  A worker's chunk is read from memory
+// at its first commit in the pass and written back at its last; in between it
+// waits in one of kHeldSlots register slots.  When no slot is free the chunk
+// is written back and re-read, which is only valid if the re-read is at least
+// depth commits later: the prefetch for commit j + depth is issued right after
+// commit j's store.  A nearer repeat that finds no free slot takes the slot of
+// the held chunk whose next use is furthest away, if that chunk can go back to
+// memory instead (its re-read at least depth commits after its commit).  If
+// none can, the pass has to end after commit j: the function then returns
 // j + 1 and the routes are not valid; otherwise it returns k.  reads and
 // writes count the row pairs that reach memory.
-int plan_routes(const int32_t* worker, int k, uint32_t* routes, int* reads, int* writes)
+int plan_routes(const int32_t* worker, int k, int depth, uint32_t* routes, int* reads,
+                int* writes)
 {
     int next[GEM_K_MAX];
     for (int j = 0; j < k; ++j) {
@@ -178,7 +182,8 @@ int plan_routes(const int32_t* worker, int k, uint32_t* routes, int* reads, int*
             if (worker[q] == worker[j]) { next[j] = q; break; }
     }
     int held_by[GEM_K_MAX];      // slot holding commit j's chunk, or -1
-    bool busy[gemk::kHeldSlots] = {};
+    int holder[gemk::kHeldSlots];   // commit whose chunk a slot holds, or -1
+    for (int q = 0; q < gemk::kHeldSlots; ++q) holder[q] = -1;
     uint32_t src[GEM_K_MAX], dst[GEM_K_MAX];
     *reads = *writes = 0;
     for (int j = 0; j < k; ++j) {
@@ -188,34 +193,50 @@ int plan_routes(const int32_t* worker, int k, uint32_t* routes, int* reads, int*
             if (worker[q] == worker[j]) prev = q;
         if (prev >= 0 && held_by[prev] >= 0) {
             src[j] = static_cast<uint32_t>(held_by[prev]);
-            busy[held_by[prev]] = false;
+            holder[held_by[prev]] = -1;
         } else {
             src[j] = gemk::kFromRing;
             *reads += 1;
         }
         dst[j] = gemk::kToMemory;
         if (next[j] >= 0) {
-            for (int q = 0; q < gemk::kHeldSlots; ++q)
-                if (!busy[q]) {
-                    busy[q] = true;
-                    held_by[j] = q;
-                    dst[j] = static_cast<uint32_t>(q);
-                    break;
+            int slot = -1;
+            for (int q = 0; q < gemk::kHeldSlots && slot < 0; ++q)
+                if (holder[q] < 0) slot = q;
+            if (slot < 0 && next[j] - j < depth) {
+                // Evict: the held chunk used furthest ahead goes back to memory
+                // at its own commit and is read again through the ring.
+                for (int q = 0; q < gemk::kHeldSlots; ++q) {
+                    const int p = holder[q];
+                    if (next[p] - p >= depth &&
+                        (slot < 0 || next[p] > next[holder[slot]]))
+                        slot = q;
                 }
-            if (held_by[j] < 0 && next[j] - j < gemk::kPrefetchDepth) return j + 1;
+                if (slot < 0) return j + 1;
+                const int p = holder[slot];
+                dst[p] = gemk::kToMemory;
+                held_by[p] = -1;
+                *writes += 1;
+            }
+            if (slot >= 0) {
+                holder[slot] = j;
+                held_by[j] = slot;
+                dst[j] = static_cast<uint32_t>(slot);
+            }
         }
         if (dst[j] == gemk::kToMemory) *writes += 1;
     }
     for (int j = 0; j < k; ++j) {
-        const int jn = j + gemk::kPrefetchDepth;
+        const int jn = j + depth;
         const bool pf = jn < k && src[jn] == gemk::kFromRing;
         routes[j] = gemk::make_route(src[j], dst[j], pf);
     }
     return k;
 }
 
-// Cut a validated commit sequence into passes of at most Kmax commits.
-void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t Kmax,
+// Cut a validated commit sequence into passes of at most Kmax commits, with
+// routes for a ring of the given depth.
+void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t Kmax, int depth,
                  std::vector<Pass>& out)
 {
     std::vector<int64_t> pc = g->pc;
@@ -224,7 +245,8 @@ void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t 
         Pass p;
         int k = static_cast<int>(std::min<int64_t>(Kmax, T - j0));
         // A shorter pass holds fewer workers at once, so this settles quickly.
-        for (int fit; (fit = plan_routes(worker + j0, k, p.routes, &p.row_reads, &p.row_writes)) < k;)
+        for (int fit; (fit = plan_routes(worker + j0, k, depth, p.routes, &p.row_reads,
+                                         &p.row_writes)) < k;)
             k = fit;
         p.K = k;
         for (int j = 0; j < k; ++j) {
@@ -268,8 +290,18 @@ void base_args(const gem_handle* g, PassArgs& a)
 }
 
 // Queue the planned passes; advance the clock and pull bookkeeping.
+// The ring depth of a run's passes: the deep ring for the default rule with
+// per-worker moments on generated updates in passes of at least kDeepMinK
+// commits, without diagnostics or recording.
+int pass_depth(const gem_handle* g, Source src, int64_t kmax)
+{
+    const bool deep = src == Source::Generated && kernel_variant(g->hp) == gemk::Variant::Fast &&
+                      kmax >= gemk::kDeepMinK && !g->diag_on && !g->hist_on;
+    return deep ? gemk::kPrefetchDeep : gemk::kPrefetchShallow;
+}
+
 int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
-               const void* const* upd, bool bf16_out)
+               const void* const* upd, bool bf16_out, int depth)
 {
     PassArgs a;
     base_args(g, a);
@@ -301,7 +333,7 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
         a.diag = g->diag_on ? g->acc : nullptr;
         a.hist_first = g->hist_count;
         a.hist_cap = g->hist_cap;
-        GEM_HIP(gemk::launch_pass(a, src, variant, bf16_out, g->diag_on || hist, g->stream));
+        GEM_HIP(gemk::launch_pass(a, src, variant, bf16_out, g->diag_on || hist, depth, g->stream));
         if (g->hist_on) g->hist_count += p.K;
         for (int j = 0; j < p.K; ++j) g->pc[p.worker[j]] = next_pull(g, g->t + j);
         g->t += p.K;
@@ -662,9 +694,10 @@ int gem_commit_batch(gem_t* g, int32_t K, const void* const* dthetas_dev, int32_
     if (g->hp.pi_scope == GEM_PI_SEGMENT) {
         return run_segments(g, worker_ids, K, src, dthetas_dev, false);
     }
+    const int depth = pass_depth(g, src, std::min<int32_t>(K, GEM_K_MAX));
     std::vector<Pass> passes;
-    plan_passes(g, worker_ids, K, GEM_K_MAX, passes);
-    return run_passes(g, passes, src, dthetas_dev, false);
+    plan_passes(g, worker_ids, K, GEM_K_MAX, depth, passes);
+    return run_passes(g, passes, src, dthetas_dev, false, depth);
 }
 
 int gem_set_segments(gem_t* g, const int64_t* offsets, int32_t count)
@@ -709,9 +742,11 @@ int gem_sim_run(gem_t* g, const int32_t* worker, const int32_t* tau, int64_t T, 
         return run_segments(g, worker, T, Source::Generated, nullptr,
                             g->sp.update_dtype == GEM_BF16);
     }
+    const int depth = pass_depth(g, Source::Generated, std::min<int64_t>(K, T));
     std::vector<Pass> passes;
-    plan_passes(g, worker, T, K, passes);
-    return run_passes(g, passes, Source::Generated, nullptr, g->sp.update_dtype == GEM_BF16);
+    plan_passes(g, worker, T, K, depth, passes);
+    return run_passes(g, passes, Source::Generated, nullptr, g->sp.update_dtype == GEM_BF16,
+                      depth);
 }
 
 int gem_read_theta(gem_t* g, float* out, int32_t out_is_device)

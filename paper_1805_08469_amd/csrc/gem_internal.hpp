@@ -12,10 +12,16 @@ namespace gemk {
 // Bits 0-3: where the committing worker's (snapshot, moment) chunk comes from:
 // a register slot 0..kHeldSlots-1 or the prefetch ring (memory).  Bits 4-7:
 // where it goes: a register slot or memory.  Bit 8: prefetch the rows of
-// commit j + kPrefetchDepth, which reads them from memory.
+// commit j + depth, which reads them from memory.
 constexpr int kHeldSlots = 4;
-// How many commits ahead a step prefetches rows: the ring depth.
-constexpr int kPrefetchDepth = 2;
+// How many commits ahead a step prefetches rows: the ring depth.  The deep
+// ring is used by the default rule with per-worker moments on generated
+// updates, in passes of at least kDeepMinK commits and without diagnostics;
+// measured on MI355X it is 2-3% faster there, and 2-3% slower for the
+// VALU-bound variants and for short passes, whose occupancy it lowers.
+constexpr int kPrefetchShallow = 2;
+constexpr int kPrefetchDeep = 4;
+constexpr int kDeepMinK = 16;
 constexpr uint32_t kRouteSlotMask = 0xFu;
 constexpr uint32_t kRouteDstShift = 4;
 constexpr uint32_t kFromRing = 0xFu;
@@ -154,8 +160,10 @@ struct SegArgs {
 enum class Variant { General = 0, Fast = 1, FastGlobal = 2 };
 
 // Launchers (defined in gem_kernels.hip).
+// depth: kPrefetchShallow, or kPrefetchDeep for (Generated, Fast, no
+// diagnostics); the routes in a must be planned for the same depth.
 hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
-                       hipStream_t stream);
+                       int depth, hipStream_t stream);
 hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream);
 hipError_t launch_seg_blocks(const double* part, int64_t npart, const int64_t* part_off,
                              const int64_t* seg_off, const int32_t* pair_seg,

@@ -201,23 +201,23 @@ __device__ __forceinline__ Held held_put(Held h, uint32_t slot, const Rows& r)
 
 struct StepOut {
     Rows out;    // the worker's (snapshot, moment) chunk after commit j
-    Rows next;   // ring entry for commit j + kPrefetchDepth
+    Rows next;   // ring entry for commit j + DEPTH
     Held held;
 };
 
 
 // Commit j of a pass.  The committing worker's (snapshot, moment) chunk comes
-// from the prefetch ring (loaded kPrefetchDepth commits earlier: a first
-// commit in the pass, or a worker whose earlier commit in the pass, at least
-// kPrefetchDepth commits back, wrote its rows back) or from a register slot.
-// After the commit the chunk is written back (the worker's last commit in the
-// pass, or no slot was free) or held in a slot; then the rows of commit
-// j + kPrefetchDepth are prefetched into the ring entry just consumed, if that
+// from the prefetch ring (loaded DEPTH commits earlier: a first commit in the
+// pass, or a worker whose earlier commit in the pass, at least DEPTH commits
+// back, wrote its rows back) or from a register slot.  After the commit the
+// chunk is written back (the worker's last commit in the pass, or no slot was
+// free) or held in a slot; then the rows of commit j + DEPTH are prefetched
+// into the ring entry just consumed, if that
 // commit reads them from memory.  Every step issues one row-pair store and one
 // row-pair load unconditionally -- those a step does not need go to the small
 // sink buffer, which stays in cache -- so the wait for a step's rows never
 // covers the loads issued after them.
-template <Source SRC, Variant V, bool BF16, bool DIAG>
+template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH>
 __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch, Rows ring,
                                              Held held, DiagAcc& acc)
 {
@@ -295,7 +295,7 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
         *reinterpret_cast<float4*>((st ? a.S : a.sink_S) + so) = r.out.s;
         *reinterpret_cast<float4*>((st_m ? a.M : a.sink_M) + (st_m ? so : sink_off)) = r.out.m;
         const bool pf = (route & kRoutePrefetch) != 0;
-        const int jn = j + kPrefetchDepth < a.K ? j + kPrefetchDepth : j;
+        const int jn = j + DEPTH < a.K ? j + DEPTH : j;
         const int64_t lo =
             pf ? ch.tb + (static_cast<int64_t>(a.worker[jn]) << (kTileShift + 1)) : sink_off;
         const bool pf_m = pf && !global_m;
@@ -307,7 +307,7 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     return r;
 }
 
-template <Source SRC, Variant V, bool BF16, bool DIAG>
+template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH>
 __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
 {
     const int64_t nchunk = a.Pp >> 2;
@@ -331,10 +331,10 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     // The shared moment is worker 0's.
     if (global_m && ch.active) ch.mg = *reinterpret_cast<const float4*>(a.M + ch.tb);
     const int K = a.K;
-    // Ring of prefetched rows, unrolled kPrefetchDepth ways so that every entry
+    // Ring of prefetched rows, unrolled DEPTH ways so that every entry
     // is a fixed set of registers: commit j reads ring[j mod depth] and refills
     // it for commit j + depth -- no register copy of an in-flight load.
-    Rows ring[kPrefetchDepth];
+    Rows ring[DEPTH];
     Held held{};
     if (ch.active) {
         ch.th = *reinterpret_cast<const float4*>(a.theta + ch.off);
@@ -344,7 +344,7 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
         }
         const int64_t sink_off = (ch.c & a.sink_mask) * 4;
 #pragma unroll
-        for (int u = 0; u < kPrefetchDepth; ++u) {
+        for (int u = 0; u < DEPTH; ++u) {
             // Commit u reads memory iff it is the first commit of its worker
             // (u < depth); the others prefetch from the sink.
             // With the shared moment only the snapshot row is read.
@@ -358,7 +358,7 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
         }
     } else {
 #pragma unroll
-        for (int u = 0; u < kPrefetchDepth; ++u) ring[u] = Rows{};
+        for (int u = 0; u < DEPTH; ++u) ring[u] = Rows{};
     }
 
     DiagAcc acc;
@@ -388,19 +388,19 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
         }
     }
     int j = 0;
-    for (; j + kPrefetchDepth <= K; j += kPrefetchDepth) {
+    for (; j + DEPTH <= K; j += DEPTH) {
 #pragma unroll
-        for (int u = 0; u < kPrefetchDepth; ++u) {
-            const StepOut so = pass_step<SRC, V, BF16, DIAG>(a, j + u, ch, ring[u], held, acc);
+        for (int u = 0; u < DEPTH; ++u) {
+            const StepOut so = pass_step<SRC, V, BF16, DIAG, DEPTH>(a, j + u, ch, ring[u], held, acc);
             ring[u] = so.next;
             held = so.held;
         }
     }
-    // At most kPrefetchDepth - 1 commits remain.
+    // At most DEPTH - 1 commits remain.
 #pragma unroll
-    for (int u = 0; u + 1 < kPrefetchDepth; ++u) {
+    for (int u = 0; u + 1 < DEPTH; ++u) {
         if (j + u < K) {
-            const StepOut so = pass_step<SRC, V, BF16, DIAG>(a, j + u, ch, ring[u], held, acc);
+            const StepOut so = pass_step<SRC, V, BF16, DIAG, DEPTH>(a, j + u, ch, ring[u], held, acc);
             ring[u] = so.next;
             held = so.held;
         }
@@ -835,10 +835,10 @@ inline unsigned blocks_for(int64_t items) {
     return static_cast<unsigned>((items + kBlock - 1) / kBlock);
 }
 
-template <Source SRC, Variant V, bool BF16, bool DIAG>
+template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH>
 hipError_t launch_one(const PassArgs& a, hipStream_t st)
 {
-    hipLaunchKernelGGL((pass_kernel<SRC, V, BF16, DIAG>), dim3(blocks_for(a.Pp >> 2)),
+    hipLaunchKernelGGL((pass_kernel<SRC, V, BF16, DIAG, DEPTH>), dim3(blocks_for(a.Pp >> 2)),
                        dim3(kBlock), 0, st, a);
     return hipGetLastError();
 }
@@ -846,12 +846,21 @@ hipError_t launch_one(const PassArgs& a, hipStream_t st)
 template <Source SRC, Variant V, bool BF16>
 hipError_t launch_d(const PassArgs& a, bool diag, hipStream_t st)
 {
-    return diag ? launch_one<SRC, V, BF16, true>(a, st) : launch_one<SRC, V, BF16, false>(a, st);
+    return diag ? launch_one<SRC, V, BF16, true, kPrefetchShallow>(a, st)
+                : launch_one<SRC, V, BF16, false, kPrefetchShallow>(a, st);
 }
 
 template <Source SRC, bool BF16>
-hipError_t launch_fd(const PassArgs& a, Variant v, bool diag, hipStream_t st)
+hipError_t launch_fd(const PassArgs& a, Variant v, bool diag, int depth, hipStream_t st)
 {
+    if (depth == kPrefetchDeep) {
+        if constexpr (SRC == Source::Generated) {
+            if (v == Variant::Fast && !diag)
+                return launch_one<SRC, Variant::Fast, BF16, false, kPrefetchDeep>(a, st);
+        }
+        return hipErrorInvalidValue;
+    }
+    if (depth != kPrefetchShallow) return hipErrorInvalidValue;
     switch (v) {
     case Variant::Fast: return launch_d<SRC, Variant::Fast, BF16>(a, diag, st);
     case Variant::FastGlobal: return launch_d<SRC, Variant::FastGlobal, BF16>(a, diag, st);
@@ -863,16 +872,16 @@ hipError_t launch_fd(const PassArgs& a, Variant v, bool diag, hipStream_t st)
 }  // namespace
 
 hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
-                       hipStream_t stream)
+                       int depth, hipStream_t stream)
 {
     switch (src) {
     case Source::Generated:
-        return bf16_out ? launch_fd<Source::Generated, true>(a, v, diag, stream)
-                        : launch_fd<Source::Generated, false>(a, v, diag, stream);
+        return bf16_out ? launch_fd<Source::Generated, true>(a, v, diag, depth, stream)
+                        : launch_fd<Source::Generated, false>(a, v, diag, depth, stream);
     case Source::GivenF32:
-        return launch_fd<Source::GivenF32, false>(a, v, diag, stream);
+        return launch_fd<Source::GivenF32, false>(a, v, diag, depth, stream);
     case Source::GivenBF16:
-        return launch_fd<Source::GivenBF16, false>(a, v, diag, stream);
+        return launch_fd<Source::GivenBF16, false>(a, v, diag, depth, stream);
     }
     return hipErrorInvalidValue;
 }

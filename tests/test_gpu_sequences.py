@@ -61,6 +61,31 @@ def test_single_worker(env, K):
         assert g.stats().passes == -(-T // K)
 
 
+@pytest.mark.parametrize("proxy", ["local", "global"])
+def test_near_repeats_evict_far_held_rows(env, proxy):
+    """Four workers held in the register slots for a far repeat, then workers
+    that commit twice in a row: each near repeat takes the slot of the held
+    chunk used furthest ahead, which goes back to memory and is read again
+    through the ring.  No pass is cut, and the state equals the oracle."""
+    _, G = env
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n = 4133, 8
+    block = np.array([0, 1, 2, 3, 4, 4, 5, 5, 6, 6, 7, 7, 0, 1, 2, 3], np.int32)
+    worker = np.tile(block, 8)
+    tau = _taus(worker, np.zeros(n, np.int64), 0)
+    h, ts = make_problem(P, 1e-3, 1.0, 9)
+    hp = G.gem_hyperparams_default()
+    hp.proxy_mode = G.GEM_PROXY_GLOBAL if proxy == "global" else G.GEM_PROXY_LOCAL
+    st = O.State.initial(n, P)
+    with G.Gem(P, n, hp) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 6)
+        g.sim_run(worker, tau, 32)
+        O.run(O.Hyper(lr=0.01, sigma=0.1, seed=6, proxy=int(hp.proxy_mode)), P, st,
+              np.arange(P), h, ts, worker, tau)
+        _check(g, st, f"evictions ({proxy} proxy)")
+        assert g.stats().passes == worker.size // 32
+
+
 def test_no_repeats_in_a_pass(env):
     """n = 320 workers in a permuted round robin: every pass of 32 commits moves
     32 distinct workers' rows (no register slot is ever used)."""
