@@ -241,6 +241,66 @@ def test_reads_into_device_memory(env):
         assert L.gem_read_state(g.h, 0, 7, C.c_void_p(out.data_ptr()), 1) == G.GEM_EINVAL
 
 
+def test_rows_read_across_tiles_into_misaligned_device_memory(env):
+    """The snapshot and moment table is stored in tiles of 8192 parameters:
+    rows read back whole across tile edges and a ragged last tile, into host
+    memory, into device memory at a 4-byte offset, and through gem_gather."""
+    import ctypes as C
+    torch, G = env
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n = 3 * 8192 + 5, 3
+    h, ts = make_problem(P, 1e-3, 1.0, 17)
+    worker, tau = G.gem_schedule_make(n, 40, G.GEM_LAW_EXP, seed=17)
+    hp = O.Hyper(lr=0.01, sigma=0.1, seed=8)
+    st = O.State.initial(n, P)
+    O.run(hp, P, st, np.arange(P), h, ts, worker, tau)
+    L = G.lib()
+    with G.Gem(P, n) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 8)
+        g.sim_run(worker, tau, 32)
+        assert_parity("theta", g.theta(), st.theta)
+        buf = torch.full((P + 2,), -7.0, dtype=torch.float32, device="cuda")
+        out = buf[1:P + 1]                        # 4 bytes past a 256-byte boundary
+        for which, ref in ((G.GEM_SNAPSHOT, st.S), (G.GEM_MOMENT, st.M)):
+            for w in range(n):
+                assert L.gem_read_state(g.h, w, which, C.c_void_p(out.data_ptr()), 1) == G.GEM_OK
+                got = buf.cpu().numpy()
+                assert got[0] == -7.0 and got[-1] == -7.0       # nothing written outside
+                assert_parity(f"row {w} ({which})", got[1:P + 1], ref[w])
+        idx = np.array([0, 8191, 8192, 16383, 16384, 24575, 24576, P - 1], np.int64)
+        th, S, M = g.gather(idx)
+        assert np.array_equal(th, st.theta[idx])
+        assert np.array_equal(S, st.S[:, idx]) and np.array_equal(M, st.M[:, idx])
+
+
+def test_checkpoint_file_holds_contiguous_rows(env, tmp_path):
+    """gem_save writes theta, then each worker's snapshot row, then each moment
+    row as P contiguous floats, then the pull clocks, h and theta* -- the
+    file layout does not depend on the device table's tiles."""
+    torch, G = env
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n = 2 * 8192 + 77, 3
+    h, ts = make_problem(P, 1e-3, 1.0, 19)
+    worker, tau = G.gem_schedule_make(n, 50, G.GEM_LAW_EXP, seed=19)
+    path = str(tmp_path / "ck.bin")
+    with G.Gem(P, n) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 9)
+        g.sim_run(worker, tau, 16)
+        assert G.gem_save(g.h, path) == G.GEM_OK
+        theta, S, M, pc = g.theta(), g.S(), g.M(), g.pull_clocks()
+    raw = open(path, "rb").read()
+    body = (1 + 2 * n + 2) * P * 4 + 8 * n
+    hdr = len(raw) - body
+    assert hdr > 0 and raw[:8] == b"GEMCKPT2"
+    f = np.frombuffer(raw, dtype=np.float32, count=(1 + 2 * n) * P, offset=hdr).reshape(1 + 2 * n, P)
+    assert np.array_equal(f[0], theta)
+    assert np.array_equal(f[1:1 + n], S) and np.array_equal(f[1 + n:], M)
+    off = hdr + (1 + 2 * n) * P * 4
+    assert np.array_equal(np.frombuffer(raw, dtype=np.int64, count=n, offset=off), pc)
+    tail = np.frombuffer(raw, dtype=np.float32, count=2 * P, offset=off + 8 * n).reshape(2, P)
+    assert np.array_equal(tail[0], h) and np.array_equal(tail[1], ts)
+
+
 def test_diag_reset_restarts_the_sums(env):
     """gem_diag_reset zeroes the energy sums and counts; what follows sums only
     the later commits (against the oracle's per-commit diagnostics)."""
