@@ -160,80 +160,6 @@ struct Pass {
     int32_t row_writes = 0;   // and writes
 };
 
-// Routes of one pass of k commits for a kernel whose ring prefetches depth
-// commits ahead (see gem_internal.hpp).  A worker's chunk is read from memory
-// at its first commit in the pass and written back at its last; in between it
-// waits in one of kHeldSlots register slots.  When no slot is free the chunk
-// is written back and re-read, which is only valid if the re-read is at least
-// depth commits later: the prefetch for commit j + depth is issued right after
-// commit j's store.  A nearer repeat that finds no free slot takes the slot of
-// the held chunk whose next use is furthest away, if that chunk can go back to
-// memory instead (its re-read at least depth commits after its commit).  If
-// none can, the pass has to end after commit j: the function then returns
-// j + 1 and the routes are not valid; otherwise it returns k.  reads and
-// writes count the row pairs that reach memory.
-int plan_routes(const int32_t* worker, int k, int depth, uint32_t* routes, int* reads,
-                int* writes)
-{
-    int next[GEM_K_MAX];
-    for (int j = 0; j < k; ++j) {
-        next[j] = -1;
-        for (int q = j + 1; q < k; ++q)
-            if (worker[q] == worker[j]) { next[j] = q; break; }
-    }
-    int held_by[GEM_K_MAX];      // slot holding commit j's chunk, or -1
-    int holder[gemk::kHeldSlots];   // commit whose chunk a slot holds, or -1
-    for (int q = 0; q < gemk::kHeldSlots; ++q) holder[q] = -1;
-    uint32_t src[GEM_K_MAX], dst[GEM_K_MAX];
-    *reads = *writes = 0;
-    for (int j = 0; j < k; ++j) {
-        held_by[j] = -1;
-        int prev = -1;
-        for (int q = j - 1; q >= 0 && prev < 0; --q)
-            if (worker[q] == worker[j]) prev = q;
-        if (prev >= 0 && held_by[prev] >= 0) {
-            src[j] = static_cast<uint32_t>(held_by[prev]);
-            holder[held_by[prev]] = -1;
-        } else {
-            src[j] = gemk::kFromRing;
-            *reads += 1;
-        }
-        dst[j] = gemk::kToMemory;
-        if (next[j] >= 0) {
-            int slot = -1;
-            for (int q = 0; q < gemk::kHeldSlots && slot < 0; ++q)
-                if (holder[q] < 0) slot = q;
-            if (slot < 0 && next[j] - j < depth) {
-                // Evict: the held chunk used furthest ahead goes back to memory
-                // at its own commit and is read again through the ring.
-                for (int q = 0; q < gemk::kHeldSlots; ++q) {
-                    const int p = holder[q];
-                    if (next[p] - p >= depth &&
-                        (slot < 0 || next[p] > next[holder[slot]]))
-                        slot = q;
-                }
-                if (slot < 0) return j + 1;
-                const int p = holder[slot];
-                dst[p] = gemk::kToMemory;
-                held_by[p] = -1;
-                *writes += 1;
-            }
-            if (slot >= 0) {
-                holder[slot] = j;
-                held_by[j] = slot;
-                dst[j] = static_cast<uint32_t>(slot);
-            }
-        }
-        if (dst[j] == gemk::kToMemory) *writes += 1;
-    }
-    for (int j = 0; j < k; ++j) {
-        const int jn = j + depth;
-        const bool pf = jn < k && src[jn] == gemk::kFromRing;
-        routes[j] = gemk::make_route(src[j], dst[j], pf);
-    }
-    return k;
-}
-
 // Cut a validated commit sequence into passes of at most Kmax commits, with
 // routes for a ring of the given depth.
 void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t Kmax, int depth,
@@ -244,10 +170,7 @@ void plan_passes(const gem_handle* g, const int32_t* worker, int64_t T, int32_t 
     while (j0 < T) {
         Pass p;
         int k = static_cast<int>(std::min<int64_t>(Kmax, T - j0));
-        // A shorter pass holds fewer workers at once, so this settles quickly.
-        for (int fit; (fit = plan_routes(worker + j0, k, depth, p.routes, &p.row_reads,
-                                         &p.row_writes)) < k;)
-            k = fit;
+        k = gemk::plan_pass(worker + j0, k, depth, p.routes, &p.row_reads, &p.row_writes);
         p.K = k;
         for (int j = 0; j < k; ++j) {
             const int32_t w = worker[j0 + j];

@@ -5,28 +5,11 @@
 #include <stdint.h>
 
 #include "../../include/gem.h"
+#include "gem_plan.hpp"
 
 namespace gemk {
 
-// Per-commit route of a fused pass (host-planned, uniform across the grid).
-// Bits 0-3: where the committing worker's (snapshot, moment) chunk comes from:
-// a register slot 0..kHeldSlots-1 or the prefetch ring (memory).  Bits 4-7:
-// where it goes: a register slot or memory.  Bit 8: prefetch the rows of
-// commit j + depth, which reads them from memory.
-constexpr int kHeldSlots = 4;
-// How many commits ahead a step prefetches rows: the ring depth.  The deep
-// ring is used by the default rule with per-worker moments on generated
-// updates, in passes of at least kDeepMinK commits and without diagnostics;
-// measured on MI355X it is 2-3% faster there, and 2-3% slower for the
-// VALU-bound variants and for short passes, whose occupancy it lowers.
-constexpr int kPrefetchShallow = 2;
-constexpr int kPrefetchDeep = 4;
-constexpr int kDeepMinK = 16;
-constexpr uint32_t kRouteSlotMask = 0xFu;
-constexpr uint32_t kRouteDstShift = 4;
-constexpr uint32_t kFromRing = 0xFu;
-constexpr uint32_t kToMemory = 0xFu;
-constexpr uint32_t kRoutePrefetch = 1u << 8;
+static_assert(kPlanMaxK == GEM_K_MAX, "the planner handles whole passes");
 
 // Size of the sink rows, in 16-byte chunks (power of two); small enough to
 // stay resident in each XCD's L2.
@@ -54,11 +37,6 @@ __host__ __device__ __forceinline__ int64_t tile_index(int64_t n, int64_t w, int
 inline int64_t table_elems(int64_t n, int64_t Pp)
 {
     return ((Pp + kTileElems - 1) >> kTileShift) * n * 2 * kTileElems;
-}
-
-inline uint32_t make_route(uint32_t src, uint32_t dst, bool prefetch)
-{
-    return src | (dst << kRouteDstShift) | (prefetch ? kRoutePrefetch : 0u);
 }
 
 // Runtime mode bits for the general kernel variant.
