@@ -300,7 +300,7 @@ def main() -> int:
             "traffic": traffic,
             "alg_bytes_per_launch": alg_per_pass,
             "avg_launch_ms": avg_pass_s * 1e3,
-            "kernel": ("seg_step_kernel + seg_reduce_kernel" if args.pi_scope == "segment"
+            "kernel": ("seg_step_kernel + seg_blocks_kernel" if args.pi_scope == "segment"
                        else "pass_kernel<Generated, %s, depth %d>" % (variant, depth)),
             "copy_ceiling_GBps": copy_gbs,
             "frac_of_copy": achieved / copy_gbs,

@@ -60,6 +60,7 @@ struct gem_handle {
     int64_t* sup_off = nullptr;      // [nseg + 1] first index-block slot of each segment
     double* sup = nullptr;           // [3][nsup] index-block sums
     float* pi_seg = nullptr;         // [nseg]
+    uint32_t* seg_done = nullptr;    // [nseg] pair blocks finished in the running launch
     int64_t npart = 0;
     int64_t nsup = 0;
 };
@@ -282,6 +283,8 @@ void free_segments(gem_handle* g)
     (void)hipFree(g->sup_off);
     (void)hipFree(g->sup);
     (void)hipFree(g->pi_seg);
+    (void)hipFree(g->seg_done);
+    g->seg_done = nullptr;
     g->seg_off = g->part_off = g->sup_off = nullptr;
     g->gseg = g->pair_seg = g->pair_blk = nullptr;
     g->part = g->sup = nullptr;
@@ -326,7 +329,8 @@ int build_segments(gem_handle* g, const std::vector<int64_t>& off)
               hipMalloc(&g->pair_blk, pair_blk.size() * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&g->sup_off, sup_off.size() * sizeof(int64_t)) == hipSuccess &&
               hipMalloc(&g->sup, static_cast<size_t>(3 * nsup) * sizeof(double)) == hipSuccess &&
-              hipMalloc(&g->pi_seg, static_cast<size_t>(nseg) * sizeof(float)) == hipSuccess;
+              hipMalloc(&g->pi_seg, static_cast<size_t>(nseg) * sizeof(float)) == hipSuccess &&
+              hipMalloc(&g->seg_done, static_cast<size_t>(nseg) * sizeof(uint32_t)) == hipSuccess;
     if (!ok) {
         (void)hipGetLastError();
         free_segments(g);
@@ -347,6 +351,8 @@ int build_segments(gem_handle* g, const std::vector<int64_t>& off)
                                hipMemcpyHostToDevice, g->stream));
         GEM_HIP(hipMemcpyAsync(g->sup_off, sup_off.data(), sup_off.size() * sizeof(int64_t),
                                hipMemcpyHostToDevice, g->stream));
+        GEM_HIP(hipMemsetAsync(g->seg_done, 0, static_cast<size_t>(nseg) * sizeof(uint32_t),
+                               g->stream));
         GEM_HIP(hipStreamSynchronize(g->stream));
         return GEM_OK;
     }();
@@ -371,7 +377,6 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
         const int rc = build_segments(g, {0, g->P});
         if (rc) return rc;
     }
-    const int32_t nseg = static_cast<int32_t>(g->seg_host.size() - 1);
     SegArgs a;
     std::memset(&a, 0, sizeof(a));
     a.theta = g->theta;
@@ -395,9 +400,16 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
     a.sigma = g->sp.sigma;
     a.mu = g->hp.momentum;
     const float k_eff = kappa_eff(g->hp);
-    const bool literal = g->hp.pi_mode == GEM_PI_LITERAL;
     a.k_eff = k_eff;
     a.diag = g->diag_on ? g->acc : nullptr;
+    gemk::SegFactors f;
+    f.pi_seg = g->pi_seg;
+    f.k_eff = k_eff;
+    f.eps = g->hp.eps;
+    f.literal = g->hp.pi_mode == GEM_PI_LITERAL;
+    f.hist_per_seg = g->hist_seg ? 1 : 0;
+    f.hist = nullptr;
+    f.diag = a.diag;
     // Bytes per element-commit the launches move: theta read and written, the
     // committing worker's snapshot read and its pull written, the moment read
     // and written; generated updates read h and theta* and the pending
@@ -417,15 +429,13 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
         a.upd_prev = (upd && j > 0) ? upd[j - 1] : nullptr;
         a.upd_cur = upd ? upd[j] : nullptr;
         GEM_HIP(gemk::launch_seg_step(a, src, bf16_out, g->stream));
-        GEM_HIP(gemk::launch_seg_blocks(g->part, g->npart, g->part_off, g->seg_off, g->pair_seg,
-                                        g->pair_blk, g->nsup, g->sup, g->sup_off, g->stream));
         // Histogram recording: this commit's rows, while there is room.
-        uint32_t* hist = nullptr;
+        f.hist = nullptr;
         if (g->hist_on && g->hist_count < g->hist_cap)
-            hist = g->pi_hist + g->hist_count * g->hist_rows * GEM_PI_BINS;
-        GEM_HIP(gemk::launch_seg_reduce(g->sup, g->nsup, g->sup_off, nseg, g->pi_seg, k_eff,
-                                        g->hp.eps, literal, g->seg_off, hist, g->hist_seg,
-                                        a.diag, g->stream));
+            f.hist = g->pi_hist + g->hist_count * g->hist_rows * GEM_PI_BINS;
+        GEM_HIP(gemk::launch_seg_blocks(g->part, g->npart, g->part_off, g->seg_off, g->pair_seg,
+                                        g->pair_blk, g->nsup, g->sup, g->sup_off, g->seg_done, f,
+                                        g->stream));
         if (g->hist_on) g->hist_count += 1;
         if (g->diag_on) g->diag_commits += 1;
         g->pc[w] = next_pull(g, t);

@@ -143,14 +143,21 @@ enum class Variant { General = 0, Fast = 1, FastGlobal = 2 };
 hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
                        int depth, hipStream_t stream);
 hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream);
+// What the last block of each segment needs to form the segment's factor.
+struct SegFactors {
+    float* pi_seg;        // [nseg] out
+    float k_eff, eps;
+    int32_t literal;      // LITERAL pi (no clamp at zero)
+    int32_t hist_per_seg; // histogram rows: one per segment, or one per commit
+    uint32_t* hist;       // this commit's histogram rows, or null
+    double* diag;         // [4] accumulators, or null
+};
+// seg_done: [nseg] counters, zero between launches (each launch leaves them zero).
 hipError_t launch_seg_blocks(const double* part, int64_t npart, const int64_t* part_off,
                              const int64_t* seg_off, const int32_t* pair_seg,
                              const int32_t* pair_blk, int64_t npairs, double* sup,
-                             const int64_t* sup_off, hipStream_t stream);
-hipError_t launch_seg_reduce(const double* sup, int64_t nsup, const int64_t* sup_off,
-                             int32_t nseg, float* pi_seg, float k_eff, float eps, bool literal,
-                             const int64_t* seg_off, uint32_t* hist, bool hist_per_seg,
-                             double* diag, hipStream_t stream);
+                             const int64_t* sup_off, uint32_t* seg_done, const SegFactors& f,
+                             hipStream_t stream);
 hipError_t launch_generate(const float* S, int64_t nw, int32_t w, const float* h,
                            const float* ts, void* out, bool bf16, int64_t P, uint32_t t,
                            uint32_t key0, uint32_t key1, float neg_lr, float sigma,

@@ -429,12 +429,13 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
 // ---------------------------------------------------------------------------
 // Segment-norm scale factors (one pi per segment of the parameter vector).
 // A commit's pi needs sums of squares over whole segments, so each commit is
-// split in three launches: the step kernel starts commit t (forms d, m and
-// the drift, stores m, writes each 1024-index group's tree sums of squares),
+// split in two launches: the step kernel starts commit t (forms d, m and the
+// drift, stores m, writes each 1024-index group's tree sums of squares), and
 // seg_blocks_kernel adds the group sums of each 2^18-index block by the same
-// tree, and seg_reduce_kernel adds the block sums in order and forms one pi
-// per segment.  The next step kernel applies those factors (and the pull)
-// before starting the next commit, generating the pending update again.
+// tree, after which the last block of each segment adds the block sums in
+// order and forms the segment's pi.  The next step kernel applies those
+// factors (and the pull) before starting the next commit, generating the
+// pending update again.
 // ---------------------------------------------------------------------------
 
 __device__ __forceinline__ float4 f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
@@ -609,43 +610,6 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
     }
 }
 
-// The tree's upper levels: one block per (segment, aligned block of
-// kSegBlock indices) pair adds the 256 group sums of that index block -- zero
-// for groups outside the segment -- by the same adjacent-pairs tree.
-__global__ __launch_bounds__(kBlock) void seg_blocks_kernel(const double* __restrict__ part,
-                                                            int64_t npart,
-                                                            const int64_t* __restrict__ part_off,
-                                                            const int64_t* __restrict__ seg_off,
-                                                            const int32_t* __restrict__ pair_seg,
-                                                            const int32_t* __restrict__ pair_blk,
-                                                            double* __restrict__ sup, int64_t nsup,
-                                                            const int64_t* __restrict__ sup_off)
-{
-    static_assert(kBlock * kSegGroup == kSegBlock, "one thread per group of an index block");
-    __shared__ double lds[3][4];
-    const int32_t seg = pair_seg[blockIdx.x];
-    const int64_t blk = pair_blk[blockIdx.x];
-    const int64_t g_lo = seg_off[seg] / kSegGroup;
-    const int64_t g_hi = (seg_off[seg + 1] - 1) / kSegGroup;
-    const int64_t grp = blk * kBlock + threadIdx.x;
-    double va = 0.0, vm = 0.0, vd = 0.0;
-    if (grp >= g_lo && grp <= g_hi) {
-        const int64_t q = part_off[seg] + (grp - g_lo);
-        va = part[q];
-        vm = part[npart + q];
-        vd = part[2 * npart + q];
-    }
-    const double sa = block_tree_sum(va, lds[0]);
-    const double sm = block_tree_sum(vm, lds[1]);
-    const double sd = block_tree_sum(vd, lds[2]);
-    if (threadIdx.x == 0) {
-        const int64_t q = sup_off[seg] + (blk - seg_off[seg] / kSegBlock);
-        sup[q] = sa;
-        sup[nsup + q] = sm;
-        sup[2 * nsup + q] = sd;
-    }
-}
-
 // Lane k's binary64 value, read by every lane (the two halves through the
 // scalar unit).
 __device__ __forceinline__ double read_lane(double v, int k)
@@ -656,20 +620,16 @@ __device__ __forceinline__ double read_lane(double v, int k)
     return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
 }
 
-// One wave per segment: add the segment's index-block sums in increasing
-// order (the lanes load 64 at a time; the additions stay in order, on values
-// read lane by lane), take the norms (binary64 square root, rounded to
-// binary32) and form pi as in the element step (eq. 18 with norms).
-__global__ __launch_bounds__(64) void seg_reduce_kernel(const double* __restrict__ sup,
-                                                        int64_t nsup,
-                                                        const int64_t* __restrict__ sup_off,
-                                                        float* __restrict__ pi_seg,
-                                                        float k_eff, float eps, int32_t literal,
-                                                        const int64_t* __restrict__ seg_off,
-                                                        uint32_t* __restrict__ hist,
-                                                        int32_t hist_per_seg, double* diag)
+// One wave (threadIdx.x < 64): add segment seg's index-block sums in
+// increasing order (the lanes load 64 at a time; the additions stay in
+// order, on values read lane by lane), take the norms (binary64 square root,
+// rounded to binary32) and form pi as in the element step (eq. 18 with norms).
+__device__ void reduce_segment(int32_t seg, const double* sup, int64_t nsup,
+                               const int64_t* __restrict__ sup_off, float* __restrict__ pi_seg,
+                               float k_eff, float eps, int32_t literal,
+                               const int64_t* __restrict__ seg_off, uint32_t* hist,
+                               int32_t hist_per_seg, double* diag)
 {
-    const int32_t seg = blockIdx.x;
     const int64_t q0 = sup_off[seg], q1 = sup_off[seg + 1];
     double sa = 0.0, sm = 0.0, sd = 0.0;
     for (int64_t base = q0; base < q1; base += 64) {
@@ -707,6 +667,61 @@ __global__ __launch_bounds__(64) void seg_reduce_kernel(const double* __restrict
         uint32_t* row = hist + (hist_per_seg ? static_cast<int64_t>(seg) * GEM_PI_BINS : 0);
         atomicAdd(&row[scale_bin(pi)], static_cast<uint32_t>(seg_off[seg + 1] - seg_off[seg]));
     }
+}
+
+// The tree's upper levels and the factors: one block per (segment, aligned
+// block of kSegBlock indices) pair adds the 256 group sums of that index
+// block -- zero for groups outside the segment -- by the same adjacent-pairs
+// tree.  The last of a segment's pair blocks to finish (a device-scope
+// counter per segment, its sums released and acquired by device fences)
+// then reduces the segment's index-block sums and forms its factor; it also
+// resets the counter for the next launch.  Which block is last does not
+// change any sum: each is taken in one fixed order.
+__global__ __launch_bounds__(kBlock) void seg_blocks_kernel(const double* __restrict__ part,
+                                                            int64_t npart,
+                                                            const int64_t* __restrict__ part_off,
+                                                            const int64_t* __restrict__ seg_off,
+                                                            const int32_t* __restrict__ pair_seg,
+                                                            const int32_t* __restrict__ pair_blk,
+                                                            double* sup, int64_t nsup,
+                                                            const int64_t* __restrict__ sup_off,
+                                                            uint32_t* seg_done, SegFactors f)
+{
+    static_assert(kBlock * kSegGroup == kSegBlock, "one thread per group of an index block");
+    __shared__ double lds[3][4];
+    __shared__ int last;
+    const int32_t seg = pair_seg[blockIdx.x];
+    const int64_t blk = pair_blk[blockIdx.x];
+    const int64_t g_lo = seg_off[seg] / kSegGroup;
+    const int64_t g_hi = (seg_off[seg + 1] - 1) / kSegGroup;
+    const int64_t grp = blk * kBlock + threadIdx.x;
+    double va = 0.0, vm = 0.0, vd = 0.0;
+    if (grp >= g_lo && grp <= g_hi) {
+        const int64_t q = part_off[seg] + (grp - g_lo);
+        va = part[q];
+        vm = part[npart + q];
+        vd = part[2 * npart + q];
+    }
+    const double sa = block_tree_sum(va, lds[0]);
+    const double sm = block_tree_sum(vm, lds[1]);
+    const double sd = block_tree_sum(vd, lds[2]);
+    if (threadIdx.x == 0) {
+        const int64_t q = sup_off[seg] + (blk - seg_off[seg] / kSegBlock);
+        sup[q] = sa;
+        sup[nsup + q] = sm;
+        sup[2 * nsup + q] = sd;
+        __threadfence();   // release this block's sums to every XCD
+        const uint32_t pairs = static_cast<uint32_t>(sup_off[seg + 1] - sup_off[seg]);
+        const uint32_t done = atomicAdd(&seg_done[seg], 1u) + 1u;
+        last = done == pairs;
+        if (done == pairs) atomicExch(&seg_done[seg], 0u);
+    }
+    __syncthreads();
+    if (!last) return;
+    __threadfence();       // acquire the other blocks' sums
+    if (threadIdx.x < 64)
+        reduce_segment(seg, sup, nsup, sup_off, f.pi_seg, f.k_eff, f.eps, f.literal, seg_off,
+                       f.hist, f.hist_per_seg, f.diag);
 }
 
 template <bool BF16>
@@ -920,23 +935,13 @@ hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, hipStrea
 hipError_t launch_seg_blocks(const double* part, int64_t npart, const int64_t* part_off,
                              const int64_t* seg_off, const int32_t* pair_seg,
                              const int32_t* pair_blk, int64_t npairs, double* sup,
-                             const int64_t* sup_off, hipStream_t stream)
+                             const int64_t* sup_off, uint32_t* seg_done, const SegFactors& f,
+                             hipStream_t stream)
 {
     if (npairs <= 0) return hipSuccess;
     hipLaunchKernelGGL(seg_blocks_kernel, dim3(static_cast<unsigned>(npairs)), dim3(kBlock), 0,
                        stream, part, npart, part_off, seg_off, pair_seg, pair_blk, sup, npairs,
-                       sup_off);
-    return hipGetLastError();
-}
-
-hipError_t launch_seg_reduce(const double* sup, int64_t nsup, const int64_t* sup_off,
-                             int32_t nseg, float* pi_seg, float k_eff, float eps, bool literal,
-                             const int64_t* seg_off, uint32_t* hist, bool hist_per_seg,
-                             double* diag, hipStream_t stream)
-{
-    hipLaunchKernelGGL(seg_reduce_kernel, dim3(static_cast<unsigned>(nseg)), dim3(64), 0, stream,
-                       sup, nsup, sup_off, pi_seg, k_eff, eps, literal ? 1 : 0, seg_off, hist,
-                       hist_per_seg ? 1 : 0, diag);
+                       sup_off, seg_done, f);
     return hipGetLastError();
 }
 
