@@ -29,7 +29,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "parameter-commits/s (P×commits/s) + achieved HBM GB/s vs peak, P=25M n=100"
-KERNEL_SOURCES = ("gem_kernels.hip", "gem_device.hpp", "gem_internal.hpp", "gem_plan.hpp")
+KERNEL_SOURCES = ("gem_kernels.hip", "gem_device.hpp", "gem_internal.hpp", "gem_plan.hpp",
+                  "gem_layout.hpp")
 # Committed rocprofv3 counter summaries, per (workload, proxy) of the fast kernel variants.
 COUNTERS_FILES = {
     ("headline", "local"): os.path.join(ROOT, "profiles", "pass_kernel_headline_counters.md"),
