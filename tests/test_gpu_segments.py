@@ -283,6 +283,38 @@ def test_rejections(G):
         assert g.clock == 0
 
 
+def test_segment_factors_repeat_bit_for_bit(G):
+    """The last block of each segment's index-block sums forms its factor, found
+    by a device-scope counter between fences: whichever block that is, every
+    sum keeps its order.  Five runs of the same schedule on fresh handles, with
+    segments of many index blocks and segments inside one, give identical
+    state and factor histograms, equal to the oracle."""
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T = 5 * 262_144 + 777, 3, 60
+    seg = np.array([0, 100, 262_144 + 5, 262_144 + 6, 3 * 262_144 + 11, P], dtype=np.int64)
+    h, ts = make_problem(P, 1e-3, 1.0, 21)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=21)
+    hp = _hp(G)
+    runs = []
+    for r in range(5):
+        print(f"[segments repeat] run {r} P={P} nseg={seg.size - 1}", flush=True)
+        with G.Gem(P, n, hp) as g:
+            g.set_quadratic(h, ts, 0.01, 0.1, 5)
+            g.set_segments(seg)
+            G.gem_pi_hist_start_segments(g.h, T)
+            g.sim_run(worker, tau, 8)
+            runs.append((g.theta(), g.S(), g.M(),
+                         G.gem_pi_hist_read(g.h, T, segments=seg.size - 1)))
+    for r in range(1, 5):
+        for a, b in zip(runs[0], runs[r]):
+            assert np.array_equal(a, b), f"run {r} differs from run 0"
+    st = O.State.initial(n, P)
+    O.run_segments(_ohp(hp, 0.01, 0.1, 5), st, seg, worker, tau, h=h, ts=ts)
+    assert_parity("repeat theta", runs[0][0], st.theta)
+    assert_parity("repeat S", runs[0][1], st.S)
+    assert_parity("repeat M", runs[0][2], st.M)
+
+
 def test_headline_size_global_norm(G):
     """A 25M-parameter vector (the headline size) with four workers: one global
     segment and a model-like partition, a few commits, against the oracle on
