@@ -226,6 +226,11 @@ def main() -> int:
     # The library's ring depth for these passes (deep: the default rule with
     # per-worker moments in passes of at least 16 commits).
     depth = 4 if variant == "Fast" and wl.K >= 16 else 2
+    # The library streams (non-temporal accesses) when theta, h, theta* and the
+    # snapshot/moment table outgrow the 256 MiB Infinity Cache.
+    tiles = -(-(-(-wl.P // 64) * 64) // 8192)
+    state_bytes = 4 * (tiles * wl.n * 2 * 8192 + 3 * (-(-wl.P // 64) * 64))
+    streaming = state_bytes > (256 << 20)
 
     stream = torch.cuda.current_stream()
     g = G.Gem(wl.P, wl.n, hp, stream=stream.cuda_stream)
@@ -302,7 +307,8 @@ def main() -> int:
             "alg_bytes_per_launch": alg_per_pass,
             "avg_launch_ms": avg_pass_s * 1e3,
             "kernel": ("seg_step_kernel + seg_blocks_kernel" if args.pi_scope == "segment"
-                       else "pass_kernel<Generated, %s, depth %d>" % (variant, depth)),
+                       else "pass_kernel<Generated, %s, depth %d%s>"
+                       % (variant, depth, ", streaming" if streaming else "")),
             "copy_ceiling_GBps": copy_gbs,
             "frac_of_copy": achieved / copy_gbs,
         },

@@ -40,6 +40,7 @@ struct gem_handle {
     int64_t t = 0;
     std::vector<int64_t> pc;  // pull clock of each worker
     bool diag_on = false;
+    int32_t cache_policy = GEM_CACHE_AUTO;
     int64_t diag_commits = 0;
     uint32_t* pi_hist = nullptr;   // [hist_cap][GEM_PI_BINS] device counts
     int64_t hist_cap = 0;
@@ -224,9 +225,19 @@ int pass_depth(const gem_handle* g, Source src, int64_t kmax)
     return deep ? gemk::kPrefetchDeep : gemk::kPrefetchShallow;
 }
 
+// Whether the fused passes stream their accesses (GEM_CACHE_AUTO: when the
+// state they touch outgrows the Infinity Cache).
+bool stream_rows(const gem_handle* g)
+{
+    if (g->cache_policy != GEM_CACHE_AUTO) return g->cache_policy == GEM_CACHE_STREAM;
+    const int64_t bytes = 4 * (gemk::table_elems(g->n, g->Pp) + 3 * g->Pp);
+    return bytes > gemk::kInfinityCacheBytes;
+}
+
 int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
                const void* const* upd, bool bf16_out, int depth)
 {
+    const bool stream = stream_rows(g);
     PassArgs a;
     base_args(g, a);
     const gemk::Variant variant = kernel_variant(g->hp);
@@ -257,7 +268,8 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
         a.diag = g->diag_on ? g->acc : nullptr;
         a.hist_first = g->hist_count;
         a.hist_cap = g->hist_cap;
-        GEM_HIP(gemk::launch_pass(a, src, variant, bf16_out, g->diag_on || hist, depth, g->stream));
+        GEM_HIP(gemk::launch_pass(a, src, variant, bf16_out, g->diag_on || hist, depth, stream,
+                                  g->stream));
         if (g->hist_on) g->hist_count += p.K;
         for (int j = 0; j < p.K; ++j) g->pc[p.worker[j]] = next_pull(g, g->t + j);
         g->t += p.K;
@@ -906,6 +918,15 @@ int gem_stats_reset(gem_t* g)
 {
     if (!g) return GEM_EINVAL;
     g->stats = gem_stats_t{};
+    return GEM_OK;
+}
+
+int gem_set_cache_policy(gem_t* g, int32_t policy)
+{
+    if (!g) return GEM_EINVAL;
+    if (policy != GEM_CACHE_AUTO && policy != GEM_CACHE_KEEP && policy != GEM_CACHE_STREAM)
+        return GEM_EINVAL;
+    g->cache_policy = policy;
     return GEM_OK;
 }
 

@@ -117,8 +117,13 @@ enum class Variant { General = 0, Fast = 1, FastGlobal = 2 };
 // Launchers (defined in gem_kernels.hip).
 // depth: kPrefetchShallow, or kPrefetchDeep for (Generated, Fast, no
 // diagnostics); the routes in a must be planned for the same depth.
+// stream_rows: non-temporal row and vector accesses (the diagnostic variant
+// ignores it).
 hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
-                       int depth, hipStream_t stream);
+                       int depth, bool stream_rows, hipStream_t stream);
+
+// Infinity Cache of one MI355X: a state this small stays cached across passes.
+constexpr int64_t kInfinityCacheBytes = int64_t{256} << 20;
 hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream);
 // What the last block of each segment needs to form the segment's factor.
 struct SegFactors {

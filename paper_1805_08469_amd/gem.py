@@ -31,6 +31,7 @@ GEM_PULL_POST_COMMIT, GEM_PULL_PRE_COMMIT = 0, 1
 GEM_RULE_GEM, GEM_RULE_DOWNPOUR, GEM_RULE_ADAPTIVE = 0, 1, 2
 GEM_PROXY_LOCAL, GEM_PROXY_GLOBAL = 0, 1
 GEM_PI_ELEMENT, GEM_PI_SEGMENT = 0, 1
+GEM_CACHE_AUTO, GEM_CACHE_KEEP, GEM_CACHE_STREAM = 0, 1, 2
 GEM_LAW_EXP, GEM_LAW_EXP_UNIFORM_MEAN, GEM_LAW_EXP_LOGNORMAL_MEAN, GEM_LAW_PARETO = 0, 1, 2, 3
 GEM_SNAPSHOT, GEM_MOMENT = 0, 1
 GEM_K_MAX = 32
@@ -44,6 +45,7 @@ EXPORTED = (
     "gem_pull_clocks", "gem_reset_worker", "gem_diag_enable", "gem_diag_reset", "gem_diag",
     "gem_stats", "gem_stats_reset", "gem_save", "gem_load", "gem_sync", "gem_copy_f32",
     "gem_pi_hist_start", "gem_pi_hist_start_segments", "gem_pi_hist_read", "gem_set_segments",
+    "gem_set_cache_policy",
 )
 
 
@@ -122,6 +124,7 @@ def _load():
         "gem_save": (C.c_int, [vp, C.c_char_p]),
         "gem_load": (C.c_int, [vp, C.c_char_p]),
         "gem_sync": (C.c_int, [vp]),
+        "gem_set_cache_policy": (C.c_int, [vp, C.c_int32]),
         "gem_copy_f32": (C.c_int, [vp, vp, C.c_int64, vp]),
         "gem_pi_hist_start": (C.c_int, [vp, C.c_int64]),
         "gem_pi_hist_start_segments": (C.c_int, [vp, C.c_int64]),
@@ -326,6 +329,10 @@ def gem_sync(g: int) -> None:
     _check(_L.gem_sync(g), "gem_sync")
 
 
+def gem_set_cache_policy(g: int, policy: int) -> None:
+    _check(_L.gem_set_cache_policy(g, policy), "gem_set_cache_policy")
+
+
 def gem_copy_f32(src_dev: int, dst_dev: int, count: int, stream: int | None = None) -> int:
     return _L.gem_copy_f32(src_dev, dst_dev, count, stream or None)
 
@@ -362,6 +369,9 @@ class Gem:
 
     def set_segments(self, offsets):
         gem_set_segments(self.h, offsets)
+
+    def set_cache_policy(self, policy: int):
+        gem_set_cache_policy(self.h, policy)
 
     def sim_run(self, worker, tau, K):
         _check(gem_sim_run(self.h, worker, tau, K), "gem_sim_run")

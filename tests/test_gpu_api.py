@@ -58,9 +58,10 @@ def test_commit_one_by_one(env, P):
     assert_parity("M", M, st.M)
 
 
+@pytest.mark.parametrize("policy", ["keep", "stream"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("K", [1, 5, 32, 45])
-def test_commit_batch(env, dtype, K):
+def test_commit_batch(env, dtype, K, policy):
     torch, G = env
     P, n = 10_007, 3                      # n = 3: workers repeat inside every batch
     rng = np.random.default_rng(K)
@@ -76,6 +77,7 @@ def test_commit_batch(env, dtype, K):
         code = G.GEM_F32
         ref_upd = d
     with G.Gem(P, n) as g:
+        g.set_cache_policy(G.GEM_CACHE_STREAM if policy == "stream" else G.GEM_CACHE_KEEP)
         for b in range(3):
             rows = range(b * K, (b + 1) * K)
             g.commit_batch([dev[j].data_ptr() for j in rows], code, worker[b * K:(b + 1) * K],

@@ -152,6 +152,50 @@ def test_modes(G, mode, K):
     _check(out, st, mode)
 
 
+POLICY_CASES = [
+    ("default_depth4", {}, 32, False),    # Fast, ring depth 4
+    ("default_depth2", {}, 8, False),     # Fast, ring depth 2 (short passes)
+    ("global_proxy", dict(proxy=1), 32, False),
+    ("kappa2_linear", dict(kappa=2.0), 32, False),
+    ("default_bf16", {}, 16, True),
+]
+
+
+@pytest.mark.parametrize("case,mode,K,bf16", POLICY_CASES, ids=[c[0] for c in POLICY_CASES])
+def test_cache_policies_give_the_same_bits(G, case, mode, K, bf16):
+    """Streaming (non-temporal) and default-policy passes give the same state,
+    bit for bit, equal to the oracle -- every pass variant and ring depth, with
+    repeats and evictions inside passes (a small state, where AUTO keeps the
+    default policy and STREAM is forced)."""
+    P, n, T = 8192 * 2 + 77, 5, 160
+    hp = _hp(G, **mode)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=31, pull_mode=hp.pull_mode)
+    from paper_1805_08469_amd.workloads import make_problem
+    h, ts = make_problem(P, 1e-3, 1.0, 31)
+    states = {}
+    for policy in (G.GEM_CACHE_KEEP, G.GEM_CACHE_STREAM, G.GEM_CACHE_AUTO):
+        with G.Gem(P, n, hp) as g:
+            g.set_cache_policy(policy)
+            g.set_quadratic(h, ts, 0.01, 0.1, 9, bf16=bf16)
+            g.sim_run(worker, tau, K)
+            states[policy] = (g.theta(), g.S(), g.M())
+    for policy in (G.GEM_CACHE_STREAM, G.GEM_CACHE_AUTO):
+        for a, b in zip(states[G.GEM_CACHE_KEEP], states[policy]):
+            assert np.array_equal(a, b), f"{case}: policy {policy} differs"
+    st = O.State.initial(n, P)
+    O.run(_ohp(hp, 0.01, 0.1, 9, bf16), P, st, np.arange(P), h, ts, worker, tau)
+    assert_parity(f"{case} theta", states[G.GEM_CACHE_STREAM][0], st.theta)
+    assert_parity(f"{case} S", states[G.GEM_CACHE_STREAM][1], st.S)
+    assert_parity(f"{case} M", states[G.GEM_CACHE_STREAM][2], st.M)
+
+
+def test_cache_policy_rejects_unknown_values(G):
+    with G.Gem(100, 2) as g:
+        assert G.lib().gem_set_cache_policy(g.h, 3) == G.GEM_EINVAL
+        assert G.lib().gem_set_cache_policy(g.h, -1) == G.GEM_EINVAL
+        assert G.lib().gem_set_cache_policy(g.h, G.GEM_CACHE_STREAM) == G.GEM_OK
+
+
 @pytest.mark.parametrize("K", [1, 16])
 def test_bf16_updates(G, K):
     P, n, T = 5000, 10, 120
