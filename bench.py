@@ -172,6 +172,9 @@ def main() -> int:
     ap.add_argument("--kappa", type=float, default=1.0)
     ap.add_argument("--pi-scope", default="element", choices=["element", "segment"],
                     help="pi per parameter, or per segment from norms (one global segment)")
+    ap.add_argument("--cache", default="auto", choices=["auto", "keep", "stream"],
+                    help="cache policy of the passes: the library's rule (stream when the state "
+                         "outgrows the Infinity Cache), the default policy, or streaming")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle timing (profiling runs)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -230,10 +233,12 @@ def main() -> int:
     # snapshot/moment table outgrow the 256 MiB Infinity Cache.
     tiles = -(-(-(-wl.P // 64) * 64) // 8192)
     state_bytes = 4 * (tiles * wl.n * 2 * 8192 + 3 * (-(-wl.P // 64) * 64))
-    streaming = state_bytes > (256 << 20)
+    streaming = state_bytes > (256 << 20) if args.cache == "auto" else args.cache == "stream"
 
     stream = torch.cuda.current_stream()
     g = G.Gem(wl.P, wl.n, hp, stream=stream.cuda_stream)
+    g.set_cache_policy({"auto": G.GEM_CACHE_AUTO, "keep": G.GEM_CACHE_KEEP,
+                        "stream": G.GEM_CACHE_STREAM}[args.cache])
     g.set_quadratic(h, ts, wl.lr, wl.sigma, wl.seed, bf16=wl.bf16)
     torch.cuda.synchronize()
 
@@ -270,7 +275,8 @@ def main() -> int:
     alg_per_pass = stats.alg_bytes / passes
     avg_pass_s = elapsed / passes
     achieved = alg_per_pass / avg_pass_s / 1e9
-    traffic = measured_traffic(wl.name, args.proxy) if fast else None
+    # The counter summaries were taken with the library's own cache rule.
+    traffic = measured_traffic(wl.name, args.proxy) if fast and args.cache == "auto" else None
 
     result = {
         "metric": METRIC,
@@ -294,7 +300,7 @@ def main() -> int:
                            3: "pareto"}[wl.law],
             "passes_per_step": passes / args.steps,
             "rule": args.rule, "pi": args.pi, "proxy": args.proxy, "kappa": args.kappa,
-            "pi_scope": args.pi_scope,
+            "pi_scope": args.pi_scope, "cache": args.cache,
             "parallelism": "single-gpu",
         },
         "roofline": {
@@ -306,8 +312,8 @@ def main() -> int:
             "traffic": traffic,
             "alg_bytes_per_launch": alg_per_pass,
             "avg_launch_ms": avg_pass_s * 1e3,
-            "kernel": ("seg_step_kernel + seg_blocks_kernel" if args.pi_scope == "segment"
-                       else "pass_kernel<Generated, %s, depth %d%s>"
+            "kernel": (("seg_step_kernel + seg_blocks_kernel" + (", streaming" if streaming else ""))
+                       if args.pi_scope == "segment" else "pass_kernel<Generated, %s, depth %d%s>"
                        % (variant, depth, ", streaming" if streaming else "")),
             "copy_ceiling_GBps": copy_gbs,
             "frac_of_copy": achieved / copy_gbs,

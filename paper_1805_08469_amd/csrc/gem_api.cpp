@@ -440,7 +440,7 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
         a.t = static_cast<uint32_t>(t);
         a.upd_prev = (upd && j > 0) ? upd[j - 1] : nullptr;
         a.upd_cur = upd ? upd[j] : nullptr;
-        GEM_HIP(gemk::launch_seg_step(a, src, bf16_out, g->stream));
+        GEM_HIP(gemk::launch_seg_step(a, src, bf16_out, stream_rows(g), g->stream));
         // Histogram recording: this commit's rows, while there is room.
         f.hist = nullptr;
         if (g->hist_on && g->hist_count < g->hist_cap)
@@ -463,7 +463,7 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
     a.m_row_prev = a.m_row;
     a.upd_prev = upd ? upd[T - 1] : nullptr;
     a.upd_cur = nullptr;
-    GEM_HIP(gemk::launch_seg_step(a, src, bf16_out, g->stream));
+    GEM_HIP(gemk::launch_seg_step(a, src, bf16_out, stream_rows(g), g->stream));
     return GEM_OK;
 }
 

@@ -124,7 +124,9 @@ hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, 
 
 // Infinity Cache of one MI355X: a state this small stays cached across passes.
 constexpr int64_t kInfinityCacheBytes = int64_t{256} << 20;
-hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream);
+// stream_rows as for launch_pass (the diagnostic variant ignores it).
+hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, bool stream_rows,
+                           hipStream_t stream);
 // What the last block of each segment needs to form the segment's factor.
 struct SegFactors {
     float* pi_seg;        // [nseg] out

@@ -494,7 +494,7 @@ __device__ __forceinline__ double block_tree_sum(double v, double* lds)
     return r;
 }
 
-template <Source SRC, bool BF16, bool DIAG>
+template <Source SRC, bool BF16, bool DIAG, bool NT>
 __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
 {
     static_assert(kBlock * 4 == kSegGroup, "one block per group of sums");
@@ -505,12 +505,12 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
     const int64_t off = c * 4;
     const int32_t s_first = a.gseg[grp];
 
-    float4 th = active ? f4(a.theta + off) : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 th = active ? load4<NT>(a.theta + off) : make_float4(0.f, 0.f, 0.f, 0.f);
     const float4 th_old = th;
     float4 hv = make_float4(0.f, 0.f, 0.f, 0.f), tv = hv;
     if (SRC == Source::Generated && active) {
-        hv = f4(a.h + off);
-        tv = f4(a.ts + off);
+        hv = load4<NT>(a.h + off);
+        tv = load4<NT>(a.ts + off);
     }
     double ek = 0.0, proxy = 0.0;   // diagnostic variant: energies of the pending commit
     if (a.apply && active) {
@@ -519,7 +519,7 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
         float4 d;
         float* srow = a.S + tile_index(a.nw, a.w_prev, off);
         float4 sp = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (SRC == Source::Generated || DIAG) sp = f4(srow);
+        if (SRC == Source::Generated || DIAG) sp = load4<NT>(srow);
         if (SRC == Source::Generated) {
             const float4 z = normals4(static_cast<uint64_t>(c), a.t - 1u, a.key0, a.key1);
             d.x = stale_update<BF16>(a.neg_lr, a.sigma, sp.x, hv.x, tv.x, z.x);
@@ -539,7 +539,7 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
         if (off + 1 < a.P) th.y = __builtin_fmaf(factor(off + 1), d.y, th.y);
         if (off + 2 < a.P) th.z = __builtin_fmaf(factor(off + 2), d.z, th.z);
         if (off + 3 < a.P) th.w = __builtin_fmaf(factor(off + 3), d.w, th.w);
-        *reinterpret_cast<float4*>(srow) = pick(a.pre_pull, th_old, th);
+        store4<NT>(srow, pick(a.pre_pull, th_old, th));
         if (DIAG) {
             // E_k against the worker's snapshot (eq. 11) and the proxy energy
             // (eq. 22) of the pending commit, whose moment is already stored.
@@ -564,7 +564,7 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
         }
     }
     if (!a.start) {
-        if (active) *reinterpret_cast<float4*>(a.theta + off) = th;
+        if (active) store4<NT>(a.theta + off, th);
         return;
     }
 
@@ -574,7 +574,7 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
     d = mo;
     if (active) {
         if (a.apply && a.w_cur == a.w_prev) s = pick(a.pre_pull, th_old, th);   // just pulled
-        else s = f4(a.S + tile_index(a.nw, a.w_cur, off));
+        else s = load4<NT>(a.S + tile_index(a.nw, a.w_cur, off));
         if (SRC == Source::Generated) {
             const float4 z = normals4(static_cast<uint64_t>(c), a.t, a.key0, a.key1);
             d.x = stale_update<BF16>(a.neg_lr, a.sigma, s.x, hv.x, tv.x, z.x);
@@ -585,14 +585,14 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
             d = load_given<SRC>(a.upd_cur, c, a.P);
         }
         float* mrow = a.M + tile_index(a.nw, a.m_row, off);
-        mo = f4(mrow);
+        mo = load4<NT>(mrow);
         float4 m;
         m.x = __builtin_fmaf(a.mu, mo.x, d.x);     // Alg. 1: m <- mu m + dtheta
         m.y = __builtin_fmaf(a.mu, mo.y, d.y);
         m.z = __builtin_fmaf(a.mu, mo.z, d.z);
         m.w = __builtin_fmaf(a.mu, mo.w, d.w);
-        *reinterpret_cast<float4*>(mrow) = m;
-        *reinterpret_cast<float4*>(a.theta + off) = th;
+        store4<NT>(mrow, m);
+        store4<NT>(a.theta + off, th);
         mo = m;
     }
     // Terms of the sums of squares: drift theta_t - s_t (eq. 16), m and d.
@@ -933,34 +933,37 @@ hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, 
     return hipErrorInvalidValue;
 }
 
-template <bool DIAG>
+template <bool DIAG, bool NT>
 void launch_seg_step_d(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream)
 {
     const unsigned grid = blocks_for(a.Pp >> 2);
     switch (src) {
     case Source::Generated:
         if (bf16_out)
-            hipLaunchKernelGGL((seg_step_kernel<Source::Generated, true, DIAG>), dim3(grid),
+            hipLaunchKernelGGL((seg_step_kernel<Source::Generated, true, DIAG, NT>), dim3(grid),
                                dim3(kBlock), 0, stream, a);
         else
-            hipLaunchKernelGGL((seg_step_kernel<Source::Generated, false, DIAG>), dim3(grid),
+            hipLaunchKernelGGL((seg_step_kernel<Source::Generated, false, DIAG, NT>), dim3(grid),
                                dim3(kBlock), 0, stream, a);
         break;
     case Source::GivenF32:
-        hipLaunchKernelGGL((seg_step_kernel<Source::GivenF32, false, DIAG>), dim3(grid),
+        hipLaunchKernelGGL((seg_step_kernel<Source::GivenF32, false, DIAG, NT>), dim3(grid),
                            dim3(kBlock), 0, stream, a);
         break;
     case Source::GivenBF16:
-        hipLaunchKernelGGL((seg_step_kernel<Source::GivenBF16, false, DIAG>), dim3(grid),
+        hipLaunchKernelGGL((seg_step_kernel<Source::GivenBF16, false, DIAG, NT>), dim3(grid),
                            dim3(kBlock), 0, stream, a);
         break;
     }
 }
 
-hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, hipStream_t stream)
+hipError_t launch_seg_step(const SegArgs& a, Source src, bool bf16_out, bool stream_rows,
+                           hipStream_t stream)
 {
-    if (a.diag) launch_seg_step_d<true>(a, src, bf16_out, stream);
-    else launch_seg_step_d<false>(a, src, bf16_out, stream);
+    // The diagnostic variant keeps the default cache policy (one instance).
+    if (a.diag) launch_seg_step_d<true, false>(a, src, bf16_out, stream);
+    else if (stream_rows) launch_seg_step_d<false, true>(a, src, bf16_out, stream);
+    else launch_seg_step_d<false, false>(a, src, bf16_out, stream);
     return hipGetLastError();
 }
 

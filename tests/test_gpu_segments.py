@@ -315,6 +315,34 @@ def test_segment_factors_repeat_bit_for_bit(G):
     assert_parity("repeat M", runs[0][2], st.M)
 
 
+@pytest.mark.parametrize("bf16", [False, True])
+def test_cache_policies_give_the_same_bits(G, bf16):
+    """Streaming (non-temporal) and default-policy step kernels give the same
+    state, bit for bit, equal to the oracle (a small state, where AUTO keeps
+    the default policy and STREAM is forced)."""
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T = 3 * 1024 + 333, 4, 50
+    seg = _partition("ragged", P)
+    h, ts = make_problem(P, 1e-3, 1.0, 13)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=13)
+    hp = _hp(G)
+    states = {}
+    for policy in (G.GEM_CACHE_KEEP, G.GEM_CACHE_STREAM):
+        with G.Gem(P, n, hp) as g:
+            g.set_cache_policy(policy)
+            g.set_quadratic(h, ts, 0.01, 0.1, 3, bf16=bf16)
+            g.set_segments(seg)
+            g.sim_run(worker, tau, 8)
+            states[policy] = (g.theta(), g.S(), g.M())
+    for a, b in zip(states[G.GEM_CACHE_KEEP], states[G.GEM_CACHE_STREAM]):
+        assert np.array_equal(a, b)
+    st = O.State.initial(n, P)
+    O.run_segments(_ohp(hp, 0.01, 0.1, 3, bf16), st, seg, worker, tau, h=h, ts=ts)
+    assert_parity("stream theta", states[G.GEM_CACHE_STREAM][0], st.theta)
+    assert_parity("stream S", states[G.GEM_CACHE_STREAM][1], st.S)
+    assert_parity("stream M", states[G.GEM_CACHE_STREAM][2], st.M)
+
+
 def test_headline_size_global_norm(G):
     """A 25M-parameter vector (the headline size) with four workers: one global
     segment and a model-like partition, a few commits, against the oracle on
