@@ -67,6 +67,10 @@ enum { GEM_SNAPSHOT = 0, GEM_MOMENT = 1 };
 /* Largest number of commits one fused pass applies; longer batches are split. */
 #define GEM_K_MAX 32
 
+/* Largest P (and gem_gather count): launches run one thread per element or
+ * index, and 2^31 of them keep every grid within one dispatch. */
+#define GEM_P_MAX (INT64_C(1) << 31)
+
 /* ---- parameter blocks ----------------------------------------------------- */
 typedef struct gem_handle gem_t;
 
@@ -156,7 +160,8 @@ int gem_hyperparams_default(gem_hyperparams* hp);
  * stream), so work is ordered with other blocking-stream work.  The stream
  * must outlive the handle.  Device memory: 1 + 2n rows of P floats (2 more
  * once a problem is set), each row padded to a multiple of 64 elements.
- * Errors: EINVAL (P < 1, n < 1, out NULL, bad enum), ENOMEM, EHIP. */
+ * Errors: EINVAL (P < 1, P > GEM_P_MAX, n < 1, out NULL, bad enum), ENOMEM
+ * (including sizes whose byte count does not fit 64 bits), EHIP. */
 int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, gem_t** out);
 
 /* Free all device memory (after the stream drains) and the handle. */
@@ -228,7 +233,8 @@ int gem_read_state(gem_t* g, int32_t w, int32_t which, float* out, int32_t out_i
 
 /* Gather theta[idx[k]] into theta_out[k] and S[w][idx[k]], M[w][idx[k]] into
  * S_out[w * count + k], M_out[w * count + k] (all host; any output may be
- * NULL).  idx is a host array of count indices in [0, P). */
+ * NULL).  idx is a host array of count indices in [0, P); count at most
+ * GEM_P_MAX (EINVAL above).  ENOMEM if the device staging cannot be allocated. */
 int gem_gather(gem_t* g, const int64_t* idx, int64_t count, float* theta_out, float* S_out,
                float* M_out);
 
@@ -289,8 +295,9 @@ int gem_set_segments(gem_t* g, const int64_t* offsets, int32_t count);
  * kernel variant (off the timed path).  gem_pi_hist_read copies the recorded
  * histograms -- commit-major, GEM_PI_BINS uint32 counts over the P parameters
  * each -- for at most max_commits commits into out (host), sets *commits to
- * the number recorded, and stops recording.  Errors: EINVAL, ENOMEM, ESTATE
- * (read without a recording).
+ * the number recorded, and stops recording.  Errors: EINVAL (also a capacity
+ * whose byte count does not fit 64 bits), ENOMEM, ESTATE (read without a
+ * recording).
  * gem_pi_hist_start_segments records one histogram per segment of the
  * partition set by gem_set_segments (one segment if none): the per-tensor
  * median pi of the paper's supplementary figures.  Each recorded commit is

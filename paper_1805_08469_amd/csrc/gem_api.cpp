@@ -530,8 +530,10 @@ int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, ge
     if (hp) h = *hp;
     else gem_hyperparams_default(&h);
     if (!valid_hp(h)) return GEM_EINVAL;
+    if (P > GEM_P_MAX) return GEM_EINVAL;
     const int64_t Pp = (P + kRowAlign - 1) / kRowAlign * kRowAlign;
-    if (Pp / 4 > static_cast<int64_t>(UINT32_MAX) * 256) return GEM_EINVAL;
+    // The table's byte count must fit 64 bits (it can exceed any device).
+    if (n > INT64_MAX / 4 / gemk::table_elems(1, Pp)) return GEM_ENOMEM;
     gem_handle* g = new (std::nothrow) gem_handle();
     if (!g) return GEM_ENOMEM;
     g->P = P;
@@ -736,8 +738,9 @@ int gem_read_state(gem_t* g, int32_t w, int32_t which, float* out, int32_t out_i
 int gem_gather(gem_t* g, const int64_t* idx, int64_t count, float* theta_out, float* S_out,
                float* M_out)
 {
-    if (!g || count < 0 || (count > 0 && !idx)) return GEM_EINVAL;
+    if (!g || count < 0 || count > GEM_P_MAX || (count > 0 && !idx)) return GEM_EINVAL;
     if (count == 0) return GEM_OK;
+    if (count > INT64_MAX / 4 / (1 + 2 * static_cast<int64_t>(g->n))) return GEM_ENOMEM;
     for (int64_t k = 0; k < count; ++k)
         if (idx[k] < 0 || idx[k] >= g->P) return GEM_EINVAL;
     const int64_t rows = 1 + 2 * static_cast<int64_t>(g->n);
@@ -875,6 +878,7 @@ int hist_begin(gem_handle* g, int64_t capacity, int32_t rows, bool per_segment)
 int gem_pi_hist_start(gem_t* g, int64_t capacity)
 {
     if (!g || capacity < 1) return GEM_EINVAL;
+    if (capacity > INT64_MAX / (GEM_PI_BINS * 4)) return GEM_EINVAL;
     return hist_begin(g, capacity, 1, false);
 }
 

@@ -35,6 +35,7 @@ GEM_CACHE_AUTO, GEM_CACHE_KEEP, GEM_CACHE_STREAM = 0, 1, 2
 GEM_LAW_EXP, GEM_LAW_EXP_UNIFORM_MEAN, GEM_LAW_EXP_LOGNORMAL_MEAN, GEM_LAW_PARETO = 0, 1, 2, 3
 GEM_SNAPSHOT, GEM_MOMENT = 0, 1
 GEM_K_MAX = 32
+GEM_P_MAX = 1 << 31
 GEM_PI_BINS = 643
 
 # Every symbol include/gem.h declares.

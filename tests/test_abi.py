@@ -100,7 +100,16 @@ def test_create_rejects_bad_arguments_before_device_work():
     hp.kappa_mode = G.GEM_KAPPA_SQRT
     hp.kappa = -1.0
     assert L.gem_create(16, 4, C.byref(hp), None, C.byref(out)) == G.GEM_EINVAL
+    # sizes: P above the largest grid, and a table whose byte count wraps 64 bits
+    assert L.gem_create(G.GEM_P_MAX + 1, 1, None, None, C.byref(out)) == G.GEM_EINVAL
+    assert L.gem_create(G.GEM_P_MAX, 2**31 - 1, None, None, C.byref(out)) == G.GEM_ENOMEM
     assert out.value is None
+
+
+def test_p_max_matches_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define GEM_P_MAX \(INT64_C\(1\) << (\d+)\)", text)
+    assert m and G.GEM_P_MAX == 1 << int(m.group(1))
 
 
 def test_null_handle_calls_fail_cleanly():

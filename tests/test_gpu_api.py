@@ -2,6 +2,8 @@
 (gem_commit, gem_commit_batch in fp32 and bf16), of the generator-then-commit
 pipeline, and of the error paths: a rejected call must leave the state and
 the clock untouched."""
+import ctypes as C
+
 import numpy as np
 import pytest
 
@@ -160,6 +162,13 @@ def test_rejected_calls_change_nothing(env):
         assert G.gem_sim_run(g.h, [0], [0], 33) == G.GEM_EINVAL         # K > GEM_K_MAX
         assert G.gem_sim_run(g.h, [0, 9], None, 4) == G.GEM_EWORKER
         assert G.gem_reset_worker(g.h, 5) == G.GEM_EWORKER
+        # sizes whose byte counts would wrap: refused before any allocation
+        L = G.lib()
+        assert L.gem_pi_hist_start(g.h, 2**62) == G.GEM_EINVAL
+        assert L.gem_pi_hist_start_segments(g.h, 2**62) == G.GEM_EINVAL
+        idx = np.zeros(4, np.int64)
+        assert L.gem_gather(g.h, idx.ctypes.data_as(C.POINTER(C.c_int64)), G.GEM_P_MAX + 1,
+                            None, None, None) == G.GEM_EINVAL
         after = (g.theta(), g.S(), g.M(), g.clock, g.pull_clocks())
     for x, y in zip(before, after):
         assert np.array_equal(x, y)
