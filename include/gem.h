@@ -323,7 +323,8 @@ int gem_stats_reset(gem_t* g);
 /* Checkpoint: write / read theta, S, M, pull clocks, t, hyper-parameters,
  * the problem (if set) and the segment partition (if set) to a host file.
  * Load requires a handle of the same P and n, and checks the whole file
- * (size, partition) before it changes any state.  Resume is bit-exact: noise
+ * (size, partition, clocks: 0 <= each pull clock <= t < 2^32) before it
+ * changes any state.  Resume is bit-exact: noise
  * is a function of (seed, t, i).  GEM_EIO for an unreadable, foreign or
  * truncated file; GEM_ENOMEM (before any file or state is touched) when the
  * device row of P' elements that stages S and M cannot be allocated.  The file

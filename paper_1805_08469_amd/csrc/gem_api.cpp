@@ -1175,6 +1175,7 @@ int gem_load(gem_t* g, const char* path)
         rc = GEM_EIO;
     if (!rc && !valid_hp(hd.hp)) rc = GEM_EIO;
     std::vector<int64_t> seg;
+    std::vector<int64_t> pc(static_cast<size_t>(g->n));
     if (!rc) {
         // The whole file must be there, and the partition valid, before any
         // state is overwritten.
@@ -1182,6 +1183,17 @@ int gem_load(gem_t* g, const char* path)
         const int64_t body = static_cast<int64_t>(sizeof(hd)) + rows * g->P * 4 + 8 * static_cast<int64_t>(g->n);
         const int64_t want = body + (hd.nseg > 0 ? 8 * (hd.nseg + 1) : 0);
         if (std::fseek(f, 0, SEEK_END) != 0 || std::ftell(f) != want) rc = GEM_EIO;
+        // The clocks: 0 <= pull clock <= t <= 2^32 - 1 (t keys the noise).
+        if (!rc && (hd.t < 0 || hd.t > static_cast<int64_t>(UINT32_MAX))) rc = GEM_EIO;
+        if (!rc) {
+            const int64_t pc_at = static_cast<int64_t>(sizeof(hd)) +
+                                  (1 + 2 * static_cast<int64_t>(g->n)) * g->P * 4;
+            if (std::fseek(f, static_cast<long>(pc_at), SEEK_SET) != 0 ||
+                std::fread(pc.data(), sizeof(int64_t), pc.size(), f) != pc.size())
+                rc = GEM_EIO;
+            for (size_t w = 0; !rc && w < pc.size(); ++w)
+                if (pc[w] < 0 || pc[w] > hd.t) rc = GEM_EIO;
+        }
         if (!rc && hd.nseg > 0) {
             seg.resize(static_cast<size_t>(hd.nseg) + 1);
             if (std::fseek(f, static_cast<long>(body), SEEK_SET) != 0 ||
@@ -1212,11 +1224,11 @@ int gem_load(gem_t* g, const char* path)
         }
     }
     std::vector<float> buf(static_cast<size_t>(g->P));
-    std::vector<int64_t> pc(static_cast<size_t>(g->n));
     if (!rc) rc = read_rows(g, f, g->theta, 1, buf);
     if (!rc) rc = read_table(g, f, g->S, stage, buf);
     if (!rc) rc = read_table(g, f, g->M, stage, buf);
-    if (!rc && std::fread(pc.data(), sizeof(int64_t), pc.size(), f) != pc.size()) rc = GEM_EIO;
+    // the pull clocks, read and checked above
+    if (!rc && std::fseek(f, static_cast<long>(8 * pc.size()), SEEK_CUR) != 0) rc = GEM_EIO;
     if (!rc && hd.have_problem) rc = read_rows(g, f, g->h, 1, buf);
     if (!rc && hd.have_problem) rc = read_rows(g, f, g->ts, 1, buf);
     std::fclose(f);

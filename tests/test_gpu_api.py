@@ -312,6 +312,52 @@ def test_checkpoint_file_holds_contiguous_rows(env, tmp_path):
     assert np.array_equal(tail[0], h) and np.array_equal(tail[1], ts)
 
 
+def test_load_refuses_damaged_files_and_keeps_the_state(env, tmp_path):
+    """gem_load checks the whole file before it writes anything: a truncated
+    file, a clock outside [0, 2^32), or a pull clock after the clock is
+    GEM_EIO, and the handle's state stays as it was."""
+    torch, G = env
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n = 3000, 3
+    h, ts = make_problem(P, 1e-3, 1.0, 23)
+    worker, tau = G.gem_schedule_make(n, 40, G.GEM_LAW_EXP, seed=23)
+    path = str(tmp_path / "ck.bin")
+    with G.Gem(P, n) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 9)
+        g.sim_run(worker, tau, 8)
+        assert G.gem_save(g.h, path) == G.GEM_OK
+    raw = bytearray(open(path, "rb").read())
+    hdr = len(raw) - ((1 + 2 * n + 2) * P * 4 + 8 * n)
+    pc_at = hdr + (1 + 2 * n) * P * 4
+    t_at = 24   # magic, P, n, have_problem, then t
+    assert int.from_bytes(raw[t_at:t_at + 8], "little", signed=True) == 40
+
+    def damaged(edit):
+        b = bytearray(raw)
+        edit(b)
+        q = str(tmp_path / "bad.bin")
+        open(q, "wb").write(bytes(b))
+        return q
+
+    bad = [
+        damaged(lambda b: b.__delitem__(slice(len(b) - 4, len(b)))),            # truncated
+        damaged(lambda b: b.__setitem__(slice(t_at, t_at + 8), (-1).to_bytes(8, "little", signed=True))),
+        damaged(lambda b: b.__setitem__(slice(t_at, t_at + 8), (2**32).to_bytes(8, "little"))),
+        damaged(lambda b: b.__setitem__(slice(pc_at, pc_at + 8), (41).to_bytes(8, "little"))),
+        damaged(lambda b: b.__setitem__(slice(pc_at + 8, pc_at + 16), (-3).to_bytes(8, "little", signed=True))),
+    ]
+    with G.Gem(P, n) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 9)
+        g.sim_run(worker[:10], tau[:10], 8)
+        before = (g.theta(), g.S(), g.M(), g.clock, g.pull_clocks())
+        for q in bad:
+            assert G.gem_load(g.h, q) == G.GEM_EIO, q
+        after = (g.theta(), g.S(), g.M(), g.clock, g.pull_clocks())
+        for x, y in zip(before, after):
+            assert np.array_equal(x, y)
+        assert G.gem_load(g.h, path) == G.GEM_OK and g.clock == 40
+
+
 def test_diag_reset_restarts_the_sums(env):
     """gem_diag_reset zeroes the energy sums and counts; what follows sums only
     the later commits (against the oracle's per-commit diagnostics)."""
