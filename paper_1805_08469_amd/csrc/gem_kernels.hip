@@ -187,13 +187,34 @@ __device__ __forceinline__ void store4(float* p, float4 v)
     }
 }
 
+// The same at a (uniform) base plus a 32-bit byte offset, which the scalar
+// base + vector offset addressing takes as is.
+template <bool NT>
+__device__ __forceinline__ float4 load4_at(const float* base, uint32_t byte_off)
+{
+    return load4<NT>(reinterpret_cast<const float*>(reinterpret_cast<const char*>(base) + byte_off));
+}
+
+template <bool NT>
+__device__ __forceinline__ void store4_at(float* base, uint32_t byte_off, float4 v)
+{
+    store4<NT>(reinterpret_cast<float*>(reinterpret_cast<char*>(base) + byte_off), v);
+}
+
 
 // Per-thread context of a fused pass: the chunk, its central values and the
 // problem coefficients, kept in registers for the whole pass.
 struct Chunk {
     int64_t c;       // chunk index (= Philox counter q of its four elements)
     int64_t off;     // element offset 4c
-    int64_t tb;      // table index of worker 0's snapshot chunk; worker w's is tb + w * 2 * kTileElems
+    // Table addresses split into a block-uniform part and a 32-bit lane part:
+    // worker w's snapshot chunk is S[tile + w * 2 * kTileElems + io], its
+    // moment chunk M[...] at the same index.
+    int64_t tile;    // table index of worker 0's snapshot piece of the block's tile
+    uint32_t io;     // byte offset of the chunk inside its tile's piece
+    uint32_t so;     // byte offset of the chunk's entries in the sink buffers
+    int64_t blk0;    // first element of the block
+    uint32_t t16;    // byte offset of the chunk from blk0 (16 * threadIdx.x)
     bool active;
     bool l0, l1, l2, l3;   // elements below the true length (diagnostics)
     int32_t sg[4];         // per-segment histograms: each element's segment
@@ -316,20 +337,18 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     r.held = held;
     if (ch.active) {
         // With the shared moment, only snapshot rows move; moment traffic goes
-        // to the sink.
-        const int64_t sink_off = (ch.c & a.sink_mask) * 4;
+        // to the sink.  Row bases are uniform; lanes add their 32-bit offset.
         const bool st = dst == kToMemory;
-        const int64_t so = st ? ch.tb + (static_cast<int64_t>(w) << (kTileShift + 1)) : sink_off;
+        const int64_t wrow = ch.tile + (static_cast<int64_t>(w) << (kTileShift + 1));
         const bool st_m = st && !global_m;
-        store4<NT>((st ? a.S : a.sink_S) + so, r.out.s);
-        store4<NT>((st_m ? a.M : a.sink_M) + (st_m ? so : sink_off), r.out.m);
+        store4_at<NT>(st ? a.S + wrow : a.sink_S, st ? ch.io : ch.so, r.out.s);
+        store4_at<NT>(st_m ? a.M + wrow : a.sink_M, st_m ? ch.io : ch.so, r.out.m);
         const bool pf = (route & kRoutePrefetch) != 0;
         const int jn = j + DEPTH < a.K ? j + DEPTH : j;
-        const int64_t lo =
-            pf ? ch.tb + (static_cast<int64_t>(a.worker[jn]) << (kTileShift + 1)) : sink_off;
+        const int64_t nrow = ch.tile + (static_cast<int64_t>(a.worker[jn]) << (kTileShift + 1));
         const bool pf_m = pf && !global_m;
-        r.next.s = load4<NT>((pf ? a.S : a.sink_S) + lo);
-        r.next.m = load4<NT>((pf_m ? a.M : a.sink_M) + (pf_m ? lo : sink_off));
+        r.next.s = load4_at<NT>(pf ? a.S + nrow : a.sink_S, pf ? ch.io : ch.so);
+        r.next.m = load4_at<NT>(pf_m ? a.M + nrow : a.sink_M, pf_m ? ch.io : ch.so);
     } else {
         r.next = ring;
     }
@@ -356,9 +375,14 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     ch.mg = ch.th;
     const bool global_m = V == Variant::FastGlobal ||
                           (V == Variant::General && (a.mode & kModeGlobalProxy));
-    ch.tb = tile_index(a.nw, 0, ch.off);
+    static_assert(kTileElems % (kBlock * 4) == 0, "a block's chunks lie in one tile");
+    ch.blk0 = static_cast<int64_t>(blockIdx.x) * (kBlock * 4);
+    ch.t16 = threadIdx.x * 16u;
+    ch.tile = tile_index(a.nw, 0, ch.blk0 & ~(kTileElems - 1));
+    ch.io = static_cast<uint32_t>(ch.blk0 & (kTileElems - 1)) * 4u + ch.t16;
+    ch.so = static_cast<uint32_t>(ch.c & a.sink_mask) * 16u;
     // The shared moment is worker 0's.
-    if (global_m && ch.active) ch.mg = load4<NT>(a.M + ch.tb);
+    if (global_m && ch.active) ch.mg = load4_at<NT>(a.M + ch.tile, ch.io);
     const int K = a.K;
     // Ring of prefetched rows, unrolled DEPTH ways so that every entry
     // is a fixed set of registers: commit j reads ring[j mod depth] and refills
@@ -366,12 +390,11 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     Rows ring[DEPTH];
     Held held{};
     if (ch.active) {
-        ch.th = load4<NT>(a.theta + ch.off);
+        ch.th = load4_at<NT>(a.theta + ch.blk0, ch.t16);
         if (SRC == Source::Generated) {
-            ch.hh = load4<NT>(a.h + ch.off);
-            ch.tt = load4<NT>(a.ts + ch.off);
+            ch.hh = load4_at<NT>(a.h + ch.blk0, ch.t16);
+            ch.tt = load4_at<NT>(a.ts + ch.blk0, ch.t16);
         }
-        const int64_t sink_off = (ch.c & a.sink_mask) * 4;
 #pragma unroll
         for (int u = 0; u < DEPTH; ++u) {
             // Commit u reads memory iff it is the first commit of its worker
@@ -379,10 +402,9 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
             // With the shared moment only the snapshot row is read.
             const bool mem = u < K && (a.routes[u] & kRouteSlotMask) == kFromRing;
             const bool mem_m = mem && !global_m;
-            const int64_t lo =
-                mem ? ch.tb + (static_cast<int64_t>(a.worker[u]) << (kTileShift + 1)) : sink_off;
-            ring[u].s = load4<NT>((mem ? a.S : a.sink_S) + lo);
-            ring[u].m = load4<NT>((mem_m ? a.M : a.sink_M) + (mem_m ? lo : sink_off));
+            const int64_t wrow = ch.tile + (static_cast<int64_t>(a.worker[u]) << (kTileShift + 1));
+            ring[u].s = load4_at<NT>(mem ? a.S + wrow : a.sink_S, mem ? ch.io : ch.so);
+            ring[u].m = load4_at<NT>(mem_m ? a.M + wrow : a.sink_M, mem_m ? ch.io : ch.so);
         }
     } else {
 #pragma unroll
@@ -433,8 +455,8 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
             held = so.held;
         }
     }
-    if (ch.active) store4<NT>(a.theta + ch.off, ch.th);
-    if (global_m && ch.active) store4<NT>(a.M + ch.tb, ch.mg);
+    if (ch.active) store4_at<NT>(a.theta + ch.blk0, ch.t16, ch.th);
+    if (global_m && ch.active) store4_at<NT>(a.M + ch.tile, ch.io, ch.mg);
 
     if (DIAG && a.diag) {
         __shared__ double red[4][kBlock];
