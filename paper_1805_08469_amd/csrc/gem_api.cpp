@@ -62,6 +62,7 @@ struct gem_handle {
     double* sup = nullptr;           // [3][nsup] index-block sums
     float* pi_seg = nullptr;         // [nseg]
     uint32_t* seg_done = nullptr;    // [nseg] pair blocks finished in the running launch
+    uint32_t deep_lds = 0;           // LDS reserved per block of the deep-ring pass
     int64_t npart = 0;
     int64_t nsup = 0;
 };
@@ -269,7 +270,7 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
         a.hist_first = g->hist_count;
         a.hist_cap = g->hist_cap;
         GEM_HIP(gemk::launch_pass(a, src, variant, bf16_out, g->diag_on || hist, depth, stream,
-                                  g->stream));
+                                  g->deep_lds, g->stream));
         if (g->hist_on) g->hist_count += p.K;
         for (int j = 0; j < p.K; ++j) g->pc[p.worker[j]] = next_pull(g, g->t + j);
         g->t += p.K;
@@ -548,6 +549,14 @@ int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, ge
             delete g;
             return GEM_EHIP;
         }
+    }
+    {
+        int lds = 0;
+        if (hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                                  g->device) == hipSuccess)
+            g->deep_lds = gemk::deep_lds_bytes(lds);
+        else
+            (void)hipGetLastError();   // no cap: the pass runs as its registers allow
     }
     // NULL is the device's null stream, which is also torch's default stream.
     g->stream = static_cast<hipStream_t>(stream);

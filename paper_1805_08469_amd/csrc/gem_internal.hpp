@@ -118,9 +118,11 @@ enum class Variant { General = 0, Fast = 1, FastGlobal = 2 };
 // depth: kPrefetchShallow, or kPrefetchDeep for (Generated, Fast, no
 // diagnostics); the routes in a must be planned for the same depth.
 // stream_rows: non-temporal row and vector accesses (the diagnostic variant
-// ignores it).
+// ignores it).  deep_lds: dynamic LDS bytes reserved per block of the
+// deep-ring pass (deep_lds_bytes), 0 for none.
 hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
-                       int depth, bool stream_rows, hipStream_t stream);
+                       int depth, bool stream_rows, uint32_t deep_lds, hipStream_t stream);
+
 
 // Infinity Cache of one MI355X: a state this small stays cached across passes.
 constexpr int64_t kInfinityCacheBytes = int64_t{256} << 20;

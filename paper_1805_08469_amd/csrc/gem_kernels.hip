@@ -188,16 +188,27 @@ __device__ __forceinline__ void store4(float* p, float4 v)
 }
 
 // The same at a (uniform) base plus a 32-bit byte offset, which the scalar
-// base + vector offset addressing takes as is.
-template <bool NT>
+// base + vector offset addressing takes as is.  FRESH gives each use its own
+// copy of the offset (an empty asm), so that the offset's widening to 64 bits
+// is not hoisted out of the pass loop: a widened offset no longer fits that
+// addressing.
+__device__ __forceinline__ uint32_t fresh(uint32_t x)
+{
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
+template <bool NT, bool FRESH = false>
 __device__ __forceinline__ float4 load4_at(const float* base, uint32_t byte_off)
 {
+    if constexpr (FRESH) byte_off = fresh(byte_off);
     return load4<NT>(reinterpret_cast<const float*>(reinterpret_cast<const char*>(base) + byte_off));
 }
 
-template <bool NT>
+template <bool NT, bool FRESH = false>
 __device__ __forceinline__ void store4_at(float* base, uint32_t byte_off, float4 v)
 {
+    if constexpr (FRESH) byte_off = fresh(byte_off);
     store4<NT>(reinterpret_cast<float*>(reinterpret_cast<char*>(base) + byte_off), v);
 }
 
@@ -207,14 +218,19 @@ __device__ __forceinline__ void store4_at(float* base, uint32_t byte_off, float4
 struct Chunk {
     int64_t c;       // chunk index (= Philox counter q of its four elements)
     int64_t off;     // element offset 4c
-    // Table addresses split into a block-uniform part and a 32-bit lane part:
-    // worker w's snapshot chunk is S[tile + w * 2 * kTileElems + io], its
-    // moment chunk M[...] at the same index.
+    // Addresses as a block-uniform part and a 32-bit lane part: worker w's
+    // snapshot chunk is at S + tile + w * 2 * kTileElems plus io bytes (io =
+    // 4 * tin + t16), its moment chunk at M + the same; its sink entries at
+    // sink_S / sink_M plus so bytes (so = 4 * sink0 + t16); theta, h and
+    // theta* at blk0 plus t16 bytes.
     int64_t tile;    // table index of worker 0's snapshot piece of the block's tile
+    int64_t tin;     // the block's first element offset inside its tile
+    int64_t blk0;    // first element of the block
+    int64_t sink0;   // first element of the block's sink entries
     uint32_t io;     // byte offset of the chunk inside its tile's piece
     uint32_t so;     // byte offset of the chunk's entries in the sink buffers
-    int64_t blk0;    // first element of the block
-    uint32_t t16;    // byte offset of the chunk from blk0 (16 * threadIdx.x)
+    uint32_t t16;    // 16 * threadIdx.x
+    uint32_t q_lo, q_hi;   // words of the chunk index c (the Philox counter)
     bool active;
     bool l0, l1, l2, l3;   // elements below the true length (diagnostics)
     int32_t sg[4];         // per-segment histograms: each element's segment
@@ -247,6 +263,33 @@ __device__ __forceinline__ Held held_put(Held h, uint32_t slot, const Rows& r)
     default: h.h3 = r; break;
     }
     return h;
+}
+
+// One step's row access: worker w's piece of `table` if mem, else the sink.
+// The shared-moment variant (VALU-bound) keeps the base block-uniform and
+// adds the lane's 16 * threadIdx.x bytes, which saves vector instructions and
+// registers (3-4% faster); the per-worker variants (HBM-bound) select a
+// per-lane element offset, measured 0.3-4% faster for them.
+template <bool UNIFORM, bool NT>
+__device__ __forceinline__ float4 row_load(const float* table, const float* sink, bool mem,
+                                           int32_t w, const Chunk& ch)
+{
+    const int64_t wrow = ch.tile + (static_cast<int64_t>(w) << (kTileShift + 1));
+    if constexpr (UNIFORM)
+        return load4_at<NT, true>(mem ? table + wrow + ch.tin : sink + ch.sink0, ch.t16);
+    else
+        return load4_at<NT>(mem ? table + wrow : sink, mem ? ch.io : ch.so);
+}
+
+template <bool UNIFORM, bool NT>
+__device__ __forceinline__ void row_store(float* table, float* sink, bool mem, int32_t w,
+                                          const Chunk& ch, float4 v)
+{
+    const int64_t wrow = ch.tile + (static_cast<int64_t>(w) << (kTileShift + 1));
+    if constexpr (UNIFORM)
+        store4_at<NT, true>(mem ? table + wrow + ch.tin : sink + ch.sink0, ch.t16, v);
+    else
+        store4_at<NT>(mem ? table + wrow : sink, mem ? ch.io : ch.so, v);
 }
 
 struct StepOut {
@@ -283,7 +326,10 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
 
     float4 d;
     if (SRC == Source::Generated) {
-        const float4 z = normals4(static_cast<uint64_t>(ch.c), a.t0 + static_cast<uint32_t>(j),
+        // The chunk index's high word is the block's (uniform): blocks start at
+        // multiples of kBlock chunks, so adding the lane never carries into it.
+        const uint64_t q = (static_cast<uint64_t>(ch.q_hi) << 32) | ch.q_lo;
+        const float4 z = normals4(q, a.t0 + static_cast<uint32_t>(j),
                                   a.key0, a.key1);
         d.x = stale_update<BF16>(a.neg_lr, a.sigma, rows.s.x, ch.hh.x, ch.tt.x, z.x);
         d.y = stale_update<BF16>(a.neg_lr, a.sigma, rows.s.y, ch.hh.y, ch.tt.y, z.y);
@@ -337,18 +383,17 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     r.held = held;
     if (ch.active) {
         // With the shared moment, only snapshot rows move; moment traffic goes
-        // to the sink.  Row bases are uniform; lanes add their 32-bit offset.
+        // to the sink.
+        constexpr bool U = V == Variant::FastGlobal;
         const bool st = dst == kToMemory;
-        const int64_t wrow = ch.tile + (static_cast<int64_t>(w) << (kTileShift + 1));
         const bool st_m = st && !global_m;
-        store4_at<NT>(st ? a.S + wrow : a.sink_S, st ? ch.io : ch.so, r.out.s);
-        store4_at<NT>(st_m ? a.M + wrow : a.sink_M, st_m ? ch.io : ch.so, r.out.m);
+        row_store<U, NT>(a.S, a.sink_S, st, w, ch, r.out.s);
+        row_store<U, NT>(a.M, a.sink_M, st_m, w, ch, r.out.m);
         const bool pf = (route & kRoutePrefetch) != 0;
         const int jn = j + DEPTH < a.K ? j + DEPTH : j;
-        const int64_t nrow = ch.tile + (static_cast<int64_t>(a.worker[jn]) << (kTileShift + 1));
         const bool pf_m = pf && !global_m;
-        r.next.s = load4_at<NT>(pf ? a.S + nrow : a.sink_S, pf ? ch.io : ch.so);
-        r.next.m = load4_at<NT>(pf_m ? a.M + nrow : a.sink_M, pf_m ? ch.io : ch.so);
+        r.next.s = row_load<U, NT>(a.S, a.sink_S, pf, a.worker[jn], ch);
+        r.next.m = row_load<U, NT>(a.M, a.sink_M, pf_m, a.worker[jn], ch);
     } else {
         r.next = ring;
     }
@@ -365,6 +410,9 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     if (!DIAG && !ch.active) return;
     ch.c = ch.active ? c : 0;   // inactive lanes (diagnostic variant) do no memory work
     ch.off = ch.c * 4;
+    static_assert((kBlock & (kBlock - 1)) == 0, "block size a power of two");
+    ch.q_hi = static_cast<uint32_t>((static_cast<int64_t>(blockIdx.x) * kBlock) >> 32);
+    ch.q_lo = static_cast<uint32_t>(ch.c);
     ch.l0 = ch.off + 0 < a.P;
     ch.l1 = ch.off + 1 < a.P;
     ch.l2 = ch.off + 2 < a.P;
@@ -376,11 +424,14 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     const bool global_m = V == Variant::FastGlobal ||
                           (V == Variant::General && (a.mode & kModeGlobalProxy));
     static_assert(kTileElems % (kBlock * 4) == 0, "a block's chunks lie in one tile");
+    static_assert(kSinkChunks % kBlock == 0, "a block's sink entries are contiguous");
     ch.blk0 = static_cast<int64_t>(blockIdx.x) * (kBlock * 4);
     ch.t16 = threadIdx.x * 16u;
     ch.tile = tile_index(a.nw, 0, ch.blk0 & ~(kTileElems - 1));
-    ch.io = static_cast<uint32_t>(ch.blk0 & (kTileElems - 1)) * 4u + ch.t16;
-    ch.so = static_cast<uint32_t>(ch.c & a.sink_mask) * 16u;
+    ch.tin = ch.blk0 & (kTileElems - 1);
+    ch.sink0 = ((ch.blk0 >> 2) & a.sink_mask) * 4;
+    ch.io = static_cast<uint32_t>(ch.tin) * 4u + ch.t16;
+    ch.so = static_cast<uint32_t>(ch.c & a.sink_mask) * 16u;   // = 4 * sink0 + t16
     // The shared moment is worker 0's.
     if (global_m && ch.active) ch.mg = load4_at<NT>(a.M + ch.tile, ch.io);
     const int K = a.K;
@@ -402,9 +453,9 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
             // With the shared moment only the snapshot row is read.
             const bool mem = u < K && (a.routes[u] & kRouteSlotMask) == kFromRing;
             const bool mem_m = mem && !global_m;
-            const int64_t wrow = ch.tile + (static_cast<int64_t>(a.worker[u]) << (kTileShift + 1));
-            ring[u].s = load4_at<NT>(mem ? a.S + wrow : a.sink_S, mem ? ch.io : ch.so);
-            ring[u].m = load4_at<NT>(mem_m ? a.M + wrow : a.sink_M, mem_m ? ch.io : ch.so);
+            constexpr bool U = V == Variant::FastGlobal;
+            ring[u].s = row_load<U, NT>(a.S, a.sink_S, mem, a.worker[u], ch);
+            ring[u].m = row_load<U, NT>(a.M, a.sink_M, mem_m, a.worker[u], ch);
         }
     } else {
 #pragma unroll
@@ -899,11 +950,13 @@ inline unsigned blocks_for(int64_t items) {
     return static_cast<unsigned>((items + kBlock - 1) / kBlock);
 }
 
+// lds: bytes of dynamic LDS reserved per block (unused by the kernel), which
+// caps the blocks a CU holds at once.
 template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH, bool NT>
-hipError_t launch_one(const PassArgs& a, hipStream_t st)
+hipError_t launch_one(const PassArgs& a, hipStream_t st, uint32_t lds = 0)
 {
     hipLaunchKernelGGL((pass_kernel<SRC, V, BF16, DIAG, DEPTH, NT>), dim3(blocks_for(a.Pp >> 2)),
-                       dim3(kBlock), 0, st, a);
+                       dim3(kBlock), lds, st, a);
     return hipGetLastError();
 }
 
@@ -918,14 +971,15 @@ hipError_t launch_d(const PassArgs& a, bool diag, bool stream, hipStream_t st)
 
 template <Source SRC, bool BF16>
 hipError_t launch_fd(const PassArgs& a, Variant v, bool diag, int depth, bool stream,
-                     hipStream_t st)
+                     uint32_t deep_lds, hipStream_t st)
 {
     if (depth == kPrefetchDeep) {
         if constexpr (SRC == Source::Generated) {
             if (v == Variant::Fast && !diag)
-                return stream
-                           ? launch_one<SRC, Variant::Fast, BF16, false, kPrefetchDeep, true>(a, st)
-                           : launch_one<SRC, Variant::Fast, BF16, false, kPrefetchDeep, false>(a, st);
+                return stream ? launch_one<SRC, Variant::Fast, BF16, false, kPrefetchDeep, true>(
+                                    a, st, deep_lds)
+                              : launch_one<SRC, Variant::Fast, BF16, false, kPrefetchDeep, false>(
+                                    a, st, deep_lds);
         }
         return hipErrorInvalidValue;
     }
@@ -941,16 +995,19 @@ hipError_t launch_fd(const PassArgs& a, Variant v, bool diag, int depth, bool st
 }  // namespace
 
 hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
-                       int depth, bool stream_rows, hipStream_t stream)
+                       int depth, bool stream_rows, uint32_t deep_lds, hipStream_t stream)
 {
     switch (src) {
     case Source::Generated:
-        return bf16_out ? launch_fd<Source::Generated, true>(a, v, diag, depth, stream_rows, stream)
-                        : launch_fd<Source::Generated, false>(a, v, diag, depth, stream_rows, stream);
+        return bf16_out ? launch_fd<Source::Generated, true>(a, v, diag, depth, stream_rows,
+                                                             deep_lds, stream)
+                        : launch_fd<Source::Generated, false>(a, v, diag, depth, stream_rows,
+                                                              deep_lds, stream);
     case Source::GivenF32:
-        return launch_fd<Source::GivenF32, false>(a, v, diag, depth, stream_rows, stream);
+        return launch_fd<Source::GivenF32, false>(a, v, diag, depth, stream_rows, deep_lds, stream);
     case Source::GivenBF16:
-        return launch_fd<Source::GivenBF16, false>(a, v, diag, depth, stream_rows, stream);
+        return launch_fd<Source::GivenBF16, false>(a, v, diag, depth, stream_rows, deep_lds,
+                                                   stream);
     }
     return hipErrorInvalidValue;
 }

@@ -21,6 +21,21 @@ constexpr int kHeldSlots = 4;
 constexpr int kPrefetchShallow = 2;
 constexpr int kPrefetchDeep = 4;
 constexpr int kDeepMinK = 16;
+// Blocks (of 256 threads, one wave per SIMD each) a CU holds at once in the
+// deep-ring pass: measured on MI355X, its row streams run best with 3 waves
+// per SIMD (4 are 1.8% slower, 2 are 7% slower).  The kernel needs few enough
+// registers for 4, so an unused LDS reservation sets the cap: with L bytes of
+// LDS per CU, a reservation just above L / (kDeepBlocksPerCU + 1) keeps the
+// next block out, and stays far enough below L / kDeepBlocksPerCU that the
+// allocation granularity does not push out one of the three.
+constexpr int kDeepBlocksPerCU = 3;
+inline uint32_t deep_lds_bytes(int64_t lds_per_cu)
+{
+    const int64_t b = (lds_per_cu / (kDeepBlocksPerCU + 1) / 1024 + 1) * 1024;
+    const int64_t slack = 4096;   // per block, above any allocation granule
+    return (b + slack) * kDeepBlocksPerCU <= lds_per_cu ? static_cast<uint32_t>(b) : 0u;
+}
+
 constexpr uint32_t kRouteSlotMask = 0xFu;
 constexpr uint32_t kRouteDstShift = 4;
 constexpr uint32_t kFromRing = 0xFu;

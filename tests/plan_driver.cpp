@@ -173,6 +173,17 @@ int main(int argc, char** argv)
         const bool cut = t3.passes > t3.lower_bound;
         if (cut != (depth > 5)) fail("round robin of five: cuts where none are possible, or none", 0, depth);
     }
+    // The deep pass's LDS reservation admits kDeepBlocksPerCU blocks per CU
+    // and not one more, whatever the CU's LDS size; no reservation where that
+    // cannot be had.
+    for (int64_t lds : {int64_t{160} << 10, int64_t{64} << 10, int64_t{96} << 10}) {
+        const int64_t b = gemk::deep_lds_bytes(lds);
+        if (!(b > 0 && (b + 4096) * gemk::kDeepBlocksPerCU <= lds &&
+              b * (gemk::kDeepBlocksPerCU + 1) > lds))
+            fail("LDS reservation does not cap the deep pass", 0, static_cast<int>(lds >> 10));
+    }
+    if (gemk::deep_lds_bytes(0) != 0 || gemk::deep_lds_bytes(2048) != 0)
+        fail("LDS reservation on a CU without room for it", 0, 0);
     std::printf("passes %ld (lower bound %ld) commits %ld row reads %ld writes %ld distinct %ld\n",
                 tot.passes, tot.lower_bound, tot.commits, tot.reads, tot.writes, tot.distinct);
     if (g_fail) {
