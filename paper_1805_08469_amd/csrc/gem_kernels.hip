@@ -56,6 +56,56 @@ __device__ __forceinline__ int scale_bin(float x)
 // FAST: the default rule (GEM, CLAMP0, kappa_eff = 1, post-commit pull) with
 // no runtime mode tests; otherwise every mode is read from a.mode.
 // hist_row: the histogram row this element's factor counts in, or null.
+// The default rule's step on a thread's four elements (Fast variants, no
+// diagnostics): the same arithmetic as commit_element, with one range check
+// for the four quotients.  When all eight operand magnitudes lie in
+// [2^-60, 2^60], each quotient is div_rn_core -- what div_rn takes for each of
+// them; otherwise each goes through div_rn.  fmaxf / fminf skip a NaN
+// operand, which may then reach div_rn_core: its quotient is NaN there as in
+// the general division, and the clamp makes either pi = 0.
+__device__ __forceinline__ void commit4_fast(const PassArgs& a, const float4& d, const float4& s,
+                                             float4& th, float4& m, float4& snap)
+{
+    const float dv[4] = {d.x, d.y, d.z, d.w};
+    const float sv[4] = {s.x, s.y, s.z, s.w};
+    float tv[4] = {th.x, th.y, th.z, th.w};
+    float mv[4] = {m.x, m.y, m.z, m.w};
+    float num[4], den[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        mv[k] = __builtin_fmaf(a.mu, mv[k], dv[k]);                 // Alg. 1: m <- mu m + dtheta
+        const float drift = tv[k] - sv[k];                          // theta_t - s_t (eq. 16)
+        num[k] = __builtin_fabsf(mv[k]) - __builtin_fabsf(drift);
+        den[k] = __builtin_fabsf(dv[k]) + a.eps;
+    }
+    float hi = __builtin_fabsf(num[0]), lo = hi;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if (k > 0) {
+            hi = __builtin_fmaxf(hi, __builtin_fabsf(num[k]));
+            lo = __builtin_fminf(lo, __builtin_fabsf(num[k]));
+        }
+        hi = __builtin_fmaxf(hi, __builtin_fabsf(den[k]));
+        lo = __builtin_fminf(lo, __builtin_fabsf(den[k]));
+    }
+    float q[4];
+    if (lo >= 0x1p-60f && hi <= 0x1p60f) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) q[k] = div_rn_core(num[k], den[k]);
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) q[k] = div_rn(num[k], den[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const float pi = (q[k] > 0.0f) ? q[k] : 0.0f;               // eq. 18, clamped
+        tv[k] = __builtin_fmaf(pi, dv[k], tv[k]);                   // eq. 3
+    }
+    th = make_float4(tv[0], tv[1], tv[2], tv[3]);
+    snap = th;
+    m = make_float4(mv[0], mv[1], mv[2], mv[3]);
+}
+
 template <bool FAST, bool DIAG>
 __device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float d, float s,
                                                float& th, float& m, float& snap, bool live,
@@ -363,10 +413,14 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     }
     StepOut r;
     r.out.m = rows.m;
-    commit_element<FAST, DIAG>(a, tau, d.x, rows.s.x, ch.th.x, r.out.m.x, r.out.s.x, ch.active && ch.l0, acc, hrow[0]);
-    commit_element<FAST, DIAG>(a, tau, d.y, rows.s.y, ch.th.y, r.out.m.y, r.out.s.y, ch.active && ch.l1, acc, hrow[1]);
-    commit_element<FAST, DIAG>(a, tau, d.z, rows.s.z, ch.th.z, r.out.m.z, r.out.s.z, ch.active && ch.l2, acc, hrow[2]);
-    commit_element<FAST, DIAG>(a, tau, d.w, rows.s.w, ch.th.w, r.out.m.w, r.out.s.w, ch.active && ch.l3, acc, hrow[3]);
+    if constexpr (FAST && !DIAG) {
+        commit4_fast(a, d, rows.s, ch.th, r.out.m, r.out.s);
+    } else {
+        commit_element<FAST, DIAG>(a, tau, d.x, rows.s.x, ch.th.x, r.out.m.x, r.out.s.x, ch.active && ch.l0, acc, hrow[0]);
+        commit_element<FAST, DIAG>(a, tau, d.y, rows.s.y, ch.th.y, r.out.m.y, r.out.s.y, ch.active && ch.l1, acc, hrow[1]);
+        commit_element<FAST, DIAG>(a, tau, d.z, rows.s.z, ch.th.z, r.out.m.z, r.out.s.z, ch.active && ch.l2, acc, hrow[2]);
+        commit_element<FAST, DIAG>(a, tau, d.w, rows.s.w, ch.th.w, r.out.m.w, r.out.s.w, ch.active && ch.l3, acc, hrow[3]);
+    }
 
     if (DIAG && acc.hist != nullptr) {
         __syncthreads();
