@@ -639,6 +639,15 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
         hv = load4<NT>(a.h + off);
         tv = load4<NT>(a.ts + off);
     }
+    // The rows this commit starts from, loaded with the others so that the
+    // thread waits for memory once: the committing worker's snapshot (unused
+    // when it is the pending worker, whose pull is stored below) and its
+    // moment (no earlier store of this launch touches it).
+    float4 s_cur = make_float4(0.f, 0.f, 0.f, 0.f), m_cur = s_cur;
+    if (a.start && active) {
+        s_cur = load4<NT>(a.S + tile_index(a.nw, a.w_cur, off));
+        m_cur = load4<NT>(a.M + tile_index(a.nw, a.m_row, off));
+    }
     double ek = 0.0, proxy = 0.0;   // diagnostic variant: energies of the pending commit
     if (a.apply && active) {
         // The pending commit's update: the caller's, or generated again at
@@ -701,7 +710,7 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
     d = mo;
     if (active) {
         if (a.apply && a.w_cur == a.w_prev) s = pick(a.pre_pull, th_old, th);   // just pulled
-        else s = load4<NT>(a.S + tile_index(a.nw, a.w_cur, off));
+        else s = s_cur;
         if (SRC == Source::Generated) {
             const float4 z = normals4(static_cast<uint64_t>(c), a.t, a.key0, a.key1);
             d.x = stale_update<BF16>(a.neg_lr, a.sigma, s.x, hv.x, tv.x, z.x);
@@ -712,7 +721,7 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
             d = load_given<SRC>(a.upd_cur, c, a.P);
         }
         float* mrow = a.M + tile_index(a.nw, a.m_row, off);
-        mo = load4<NT>(mrow);
+        mo = m_cur;
         float4 m;
         m.x = __builtin_fmaf(a.mu, mo.x, d.x);     // Alg. 1: m <- mu m + dtheta
         m.y = __builtin_fmaf(a.mu, mo.y, d.y);
