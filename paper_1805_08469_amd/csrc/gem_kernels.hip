@@ -621,6 +621,29 @@ __device__ __forceinline__ double block_tree_sum(double v, double* lds)
     return r;
 }
 
+// Three such sums at once, each in the same order as block_tree_sum, with one
+// pair of barriers for the three.
+__device__ __forceinline__ void block_tree_sum3(double& x, double& y, double& z, double (*lds)[4])
+{
+#pragma unroll
+    for (int mask = 1; mask < 64; mask <<= 1) {
+        x = x + __shfl_xor(x, mask);
+        y = y + __shfl_xor(y, mask);
+        z = z + __shfl_xor(z, mask);
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        lds[0][wave] = x;
+        lds[1][wave] = y;
+        lds[2][wave] = z;
+    }
+    __syncthreads();
+    x = (lds[0][0] + lds[0][1]) + (lds[0][2] + lds[0][3]);
+    y = (lds[1][0] + lds[1][1]) + (lds[1][2] + lds[1][3]);
+    z = (lds[2][0] + lds[2][1]) + (lds[2][2] + lds[2][3]);
+    __syncthreads();
+}
+
 template <Source SRC, bool BF16, bool DIAG, bool NT>
 __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
 {
@@ -762,9 +785,8 @@ __global__ __launch_bounds__(kBlock) void seg_step_kernel(const SegArgs a)
             cm = (xm[0] + xm[1]) + (xm[2] + xm[3]);
             cd = (xd[0] + xd[1]) + (xd[2] + xd[3]);
         }
-        const double sa = block_tree_sum(ca, lds[0]);
-        const double sm = block_tree_sum(cm, lds[1]);
-        const double sd = block_tree_sum(cd, lds[2]);
+        double sa = ca, sm = cm, sd = cd;
+        block_tree_sum3(sa, sm, sd, lds);
         if (threadIdx.x == 0) {
             const int64_t q = a.part_off[seg] + (grp - (lo / kSegGroup));
             a.part[q] = sa;
@@ -866,9 +888,8 @@ __global__ __launch_bounds__(kBlock) void seg_blocks_kernel(const double* __rest
         vm = part[npart + q];
         vd = part[2 * npart + q];
     }
-    const double sa = block_tree_sum(va, lds[0]);
-    const double sm = block_tree_sum(vm, lds[1]);
-    const double sd = block_tree_sum(vd, lds[2]);
+    double sa = va, sm = vm, sd = vd;
+    block_tree_sum3(sa, sm, sd, lds);
     if (threadIdx.x == 0) {
         const int64_t q = sup_off[seg] + (blk - seg_off[seg] / kSegBlock);
         sup[q] = sa;
