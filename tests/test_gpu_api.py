@@ -93,6 +93,41 @@ def test_commit_batch(env, dtype, K, policy):
     assert_parity("M", M, st.M)
 
 
+EXTREMES = np.array([0.0, -0.0, 1e-45, -1e-40, 1e-30, -1e-20, 1e-10, 1.0, -1e10, 1e20, -1e30,
+                     3e38, np.inf, -np.inf, np.nan], dtype=np.float32)
+
+
+@pytest.mark.parametrize("proxy", [0, 1])
+def test_extreme_update_magnitudes(env, proxy):
+    """Caller updates of every magnitude -- zeros of both signs, subnormals,
+    values near the ends of the exponent range, infinities and NaN, mixed with
+    ordinary ones -- through the default rule's variants (per-worker and
+    shared moment): quotients outside the range of the core division take the
+    general one, element by element, and the state stays equal to the
+    oracle's (NaN compares equal to NaN)."""
+    torch, G = env
+    P, n, T, K = 8192 + 77, 3, 24, 8
+    rng = np.random.default_rng(100 + proxy)
+    d = (rng.standard_normal((T, P)) * 0.01).astype(np.float32)
+    pick = rng.random((T, P)) < 0.03
+    d[pick] = rng.choice(EXTREMES, size=int(pick.sum()))
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=7)
+    dev = _device_rows(torch, d)
+    hp = G.gem_hyperparams_default()
+    hp.proxy_mode = G.GEM_PROXY_GLOBAL if proxy else G.GEM_PROXY_LOCAL
+    with G.Gem(P, n, hp) as g:
+        for b in range(0, T, K):
+            g.commit_batch([dev[j].data_ptr() for j in range(b, b + K)], G.GEM_F32,
+                           worker[b:b + K], tau[b:b + K])
+        theta, S, M = g.theta(), g.S(), g.M()
+    st = O.State.initial(n, P)
+    O.commit_given(O.Hyper(proxy=proxy), st, worker, d, tau=tau)
+    assert np.isnan(st.theta).any() and np.isinf(st.theta).any()   # the cases are reached
+    assert_parity("theta", theta, st.theta)
+    assert_parity("S", S, st.S)
+    assert_parity("M", M, st.M)
+
+
 @pytest.mark.parametrize("K", [1, 32])
 def test_commit_batch_global_proxy(env, K):
     """Caller updates committed with the shared moment (Sec. 6): row 0 of M."""
