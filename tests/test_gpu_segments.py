@@ -343,6 +343,35 @@ def test_cache_policies_give_the_same_bits(G, bf16):
     assert_parity("stream M", states[G.GEM_CACHE_STREAM][2], st.M)
 
 
+def test_extreme_update_magnitudes(G):
+    """Caller updates of every magnitude (subnormal, huge, infinite, NaN)
+    under per-segment factors: the binary64 sums of squares overflow, turn
+    infinite or NaN in some segments and not in others, and the state stays
+    equal to the oracle's (NaN compares equal to NaN)."""
+    import torch
+    P, n, T = 3000, 3, 24
+    rng = np.random.default_rng(41)
+    d = (rng.standard_normal((T, P)) * 0.01).astype(np.float32)
+    ext = np.array([0.0, -0.0, 1e-45, -1e-40, 1e-30, 1e20, -1e30, 3e38, np.inf, -np.inf, np.nan],
+                   dtype=np.float32)
+    pick = rng.random((T, P)) < 0.002
+    d[pick] = rng.choice(ext, size=int(pick.sum()))
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=41)
+    seg = _partition("ragged", P)
+    buf, ptrs = _device_rows(torch, d)
+    hp = _hp(G)
+    with G.Gem(P, n, hp) as g:
+        g.set_segments(seg)
+        g.commit_batch(ptrs, G.GEM_F32, worker, tau)
+        torch.cuda.synchronize()
+        out = (g.theta(), g.S(), g.M(), g.pull_clocks(), g.clock, g.stats())
+    st = O.State.initial(n, P)
+    with np.errstate(all="ignore"):
+        O.run_segments(_ohp(hp, 0.0, 0.0, 0), st, seg, worker, tau, d=d)
+    assert np.isfinite(st.theta).any() and not np.isfinite(st.theta).all()
+    _check(out, st, "extremes")
+
+
 def test_headline_size_global_norm(G):
     """A 25M-parameter vector (the headline size) with four workers: one global
     segment and a model-like partition, a few commits, against the oracle on
