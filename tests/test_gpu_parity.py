@@ -152,6 +152,37 @@ def test_modes(G, mode, K):
     _check(out, st, mode)
 
 
+@pytest.mark.parametrize("mode", sorted(MODES))
+def test_modes_with_extreme_update_magnitudes(G, mode):
+    """Every mode with caller updates of every magnitude (subnormal, huge,
+    infinite, NaN) mixed into ordinary ones: the general division where an
+    operand leaves the core range, overflow to infinity, NaN from inf - inf;
+    the state equals the oracle's (NaN compares equal to NaN)."""
+    import torch
+    P, n, T, K = 4133, 3, 24, 8
+    rng = np.random.default_rng(57)
+    d = (rng.standard_normal((T, P)) * 0.01).astype(np.float32)
+    ext = np.array([0.0, -0.0, 1e-45, -1e-40, 1e-30, -1e-20, 1e-10, -1e10, 1e20, -1e30, 3e38,
+                    np.inf, -np.inf, np.nan], dtype=np.float32)
+    pick = rng.random((T, P)) < 0.03
+    d[pick] = rng.choice(ext, size=int(pick.sum()))
+    hp = _hp(G, **MODES[mode])
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=57, pull_mode=hp.pull_mode)
+    pad = np.zeros((T, -(-P // 8) * 8), dtype=np.float32)   # rows 16-byte aligned
+    pad[:, :P] = d
+    dev = torch.from_numpy(pad).cuda()
+    with G.Gem(P, n, hp) as g:
+        for b in range(0, T, K):
+            g.commit_batch([dev[j].data_ptr() for j in range(b, b + K)], G.GEM_F32,
+                           worker[b:b + K], tau[b:b + K])
+        torch.cuda.synchronize()
+        out = (g.theta(), g.S(), g.M(), g.pull_clocks(), g.clock, g.stats())
+    st = O.State.initial(n, P)
+    with np.errstate(all="ignore"):
+        O.commit_given(_ohp(hp, 0.0, 0.0, 0), st, worker, d, tau=tau)
+    _check(out, st, f"{mode} extremes")
+
+
 POLICY_CASES = [
     ("default_depth4", {}, 32, False),    # Fast, ring depth 4
     ("default_depth2", {}, 8, False),     # Fast, ring depth 2 (short passes)
