@@ -172,6 +172,9 @@ def main() -> int:
     ap.add_argument("--kappa", type=float, default=1.0)
     ap.add_argument("--pi-scope", default="element", choices=["element", "segment"],
                     help="pi per parameter, or per segment from norms (one global segment)")
+    ap.add_argument("--pi-hist", action="store_true",
+                    help="record the per-commit histograms of the scale factor during the timed "
+                         "steps (the diagnostic kernel variant)")
     ap.add_argument("--cache", default="auto", choices=["auto", "keep", "stream"],
                     help="cache policy of the passes: the library's rule (stream when the state "
                          "outgrows the Infinity Cache), the default policy, or streaming")
@@ -250,6 +253,8 @@ def main() -> int:
         step(k)
     torch.cuda.synchronize()
     G.gem_stats_reset(g.h)
+    if args.pi_hist:
+        G.gem_pi_hist_start(g.h, args.steps * wl.T)
 
     # One event at every step boundary, on the stream the passes run on: the
     # first and last bracket the timed region, the others give per-step times.
@@ -276,7 +281,8 @@ def main() -> int:
     avg_pass_s = elapsed / passes
     achieved = alg_per_pass / avg_pass_s / 1e9
     # The counter summaries were taken with the library's own cache rule.
-    traffic = measured_traffic(wl.name, args.proxy) if fast and args.cache == "auto" else None
+    traffic = (measured_traffic(wl.name, args.proxy)
+               if fast and args.cache == "auto" and not args.pi_hist else None)
 
     result = {
         "metric": METRIC,
@@ -300,7 +306,7 @@ def main() -> int:
                            3: "pareto"}[wl.law],
             "passes_per_step": passes / args.steps,
             "rule": args.rule, "pi": args.pi, "proxy": args.proxy, "kappa": args.kappa,
-            "pi_scope": args.pi_scope, "cache": args.cache,
+            "pi_scope": args.pi_scope, "cache": args.cache, "pi_hist": args.pi_hist,
             "parallelism": "single-gpu",
         },
         "roofline": {
@@ -313,7 +319,11 @@ def main() -> int:
             "alg_bytes_per_launch": alg_per_pass,
             "avg_launch_ms": avg_pass_s * 1e3,
             "kernel": (("seg_step_kernel + seg_blocks_kernel" + (", streaming" if streaming else ""))
-                       if args.pi_scope == "segment" else "pass_kernel<Generated, %s, depth %d%s>"
+                       if args.pi_scope == "segment"
+                       # recording takes the diagnostic variant: ring depth 2, default policy
+                       else "pass_kernel<Generated, %s, diagnostic, depth 2>" % variant
+                       if args.pi_hist
+                       else "pass_kernel<Generated, %s, depth %d%s>"
                        % (variant, depth, ", streaming" if streaming else "")),
             "copy_ceiling_GBps": copy_gbs,
             "frac_of_copy": achieved / copy_gbs,
