@@ -331,8 +331,10 @@ def commit_given(hp: Hyper, st: State, worker, d, tau=None, diag: bool = False,
 
 def sumsq(x, lo: int = 0, hi: int | None = None) -> float:
     """Sum of squares of x[lo:hi] in binary64, in the order that defines the
-    segment norms (see or_sumsq): adjacent-pairs tree within aligned groups of
-    1024 indices, then the groups in increasing order."""
+    segment norms (see or_sumsq): every term the exact binary64 square; the
+    adjacent-pairs tree within each aligned block of 2^18 indices (terms
+    outside [lo, hi) are zero), then the block values added in increasing
+    block order to a running total starting at zero."""
     x = np.ascontiguousarray(x, dtype=np.float32)
     hi = x.size if hi is None else hi
     return float(lib().or_sumsq(_ptr(x, C.c_float), lo, hi))

@@ -43,8 +43,13 @@
  * reductions to SGD (bit for bit) and to the heavy-ball closed form; eqs.
  * (12)-(13) as invariants of every element-commit; Philox against numpy's
  * independent Philox4x64 and published known answers; ln, sin and cos
- * exhaustively against binary64 libm; the schedule's staleness law (Sec. 1);
- * one-element segments against the element-wise commit.  Parity unpinned:
+ * exhaustively against binary64 libm; the schedule's staleness law (Sec. 1)
+ * and the per-worker mean laws (Kolmogorov-Smirnov); one-element segments
+ * against the element-wise commit; segment factors against exactly rounded
+ * norms; the energy sums (eqs. 11, 22) and clamp counts recomputed from the
+ * states around each commit, eq. 13 for one worker and eq. 12 for clamped
+ * commits; the loss on exact cases and along the SGD closed form.
+ * Parity unpinned:
  * the paper prints no trajectory at n > 1, so beyond those invariants and
  * special cases nothing but device == oracle equality pins such runs.
  */
