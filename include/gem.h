@@ -86,7 +86,11 @@ typedef struct gem_handle gem_t;
  * (gem_read_state(g, 0, GEM_MOMENT, ...) returns it).
  * pi_scope ELEMENT computes pi per parameter from absolute values (eq. 18);
  * SEGMENT computes one pi per segment of the parameter vector from Euclidean
- * norms over the segment (see gem_set_segments; GEM rule only). */
+ * norms over the segment (see gem_set_segments; GEM rule only).
+ * momentum must be finite; eps finite and > 0 (it keeps the denominator
+ * |dtheta| + eps of Alg. 1 away from zero, so an update of exactly zero
+ * leaves theta unchanged); kappa finite and > 0 in both forms.  Calls that
+ * take a gem_hyperparams return GEM_EINVAL otherwise. */
 typedef struct {
     float momentum;
     float eps;
@@ -160,7 +164,8 @@ int gem_hyperparams_default(gem_hyperparams* hp);
  * stream), so work is ordered with other blocking-stream work.  The stream
  * must outlive the handle.  Device memory: 1 + 2n rows of P floats (2 more
  * once a problem is set), each row padded to a multiple of 64 elements.
- * Errors: EINVAL (P < 1, P > GEM_P_MAX, n < 1, out NULL, bad enum), ENOMEM
+ * Errors: EINVAL (P < 1, P > GEM_P_MAX, n < 1, out NULL, bad enum or
+ * hyper-parameter value), ENOMEM
  * (including sizes whose byte count does not fit 64 bits), EHIP. */
 int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, gem_t** out);
 
@@ -237,6 +242,11 @@ int gem_read_state(gem_t* g, int32_t w, int32_t which, float* out, int32_t out_i
  * GEM_P_MAX (EINVAL above).  ENOMEM if the device staging cannot be allocated. */
 int gem_gather(gem_t* g, const int64_t* idx, int64_t count, float* theta_out, float* S_out,
                float* M_out);
+
+/* The handle's sizes: P parameters and n workers (what every host buffer of
+ * P or n elements passed to or filled by the calls here must hold).
+ * GEM_EINVAL for a NULL argument. */
+int gem_dims(gem_t* g, int64_t* P, int32_t* n);
 
 /* Current global clock t (commits applied since the last restart). */
 int gem_clock(gem_t* g, int64_t* t);

@@ -100,7 +100,12 @@ bool valid_hp(const gem_hyperparams& hp)
     if (hp.pi_scope == GEM_PI_SEGMENT && hp.rule != GEM_RULE_GEM) return false;
     if (!std::isfinite(hp.momentum) || !std::isfinite(hp.eps) || !std::isfinite(hp.kappa))
         return false;
-    if (hp.kappa_mode == GEM_KAPPA_SQRT && hp.kappa < 0.0f) return false;
+    // eps keeps the scale factor's denominator |dtheta| + eps away from zero
+    // (Alg. 1): with eps <= 0 an update of exactly zero would give pi = inf
+    // and theta = inf * 0 = NaN.  kappa scales the proxy energy (appendix B),
+    // which is positive.
+    if (!(hp.eps > 0.0f)) return false;
+    if (!(hp.kappa > 0.0f)) return false;
     return true;
 }
 
@@ -793,6 +798,14 @@ int gem_gather(gem_t* g, const int64_t* idx, int64_t count, float* theta_out, fl
     (void)hipFree(d_idx);
     (void)hipFree(d_out);
     return rc;
+}
+
+int gem_dims(gem_t* g, int64_t* P, int32_t* n)
+{
+    if (!g || !P || !n) return GEM_EINVAL;
+    *P = g->P;
+    *n = g->n;
+    return GEM_OK;
 }
 
 int gem_clock(gem_t* g, int64_t* t)

@@ -46,7 +46,7 @@ EXPORTED = (
     "gem_pull_clocks", "gem_reset_worker", "gem_diag_enable", "gem_diag_reset", "gem_diag",
     "gem_stats", "gem_stats_reset", "gem_save", "gem_load", "gem_sync", "gem_copy_f32",
     "gem_pi_hist_start", "gem_pi_hist_start_segments", "gem_pi_hist_read", "gem_set_segments",
-    "gem_set_cache_policy",
+    "gem_set_cache_policy", "gem_dims",
 )
 
 
@@ -115,6 +115,7 @@ def _load():
         "gem_read_state": (C.c_int, [vp, C.c_int32, C.c_int32, vp, C.c_int32]),
         "gem_gather": (C.c_int, [vp, i64p, C.c_int64, vp, vp, vp]),
         "gem_clock": (C.c_int, [vp, i64p]),
+        "gem_dims": (C.c_int, [vp, i64p, i32p]),
         "gem_pull_clocks": (C.c_int, [vp, i64p]),
         "gem_reset_worker": (C.c_int, [vp, C.c_int32]),
         "gem_diag_enable": (C.c_int, [vp, C.c_int32]),
@@ -185,17 +186,39 @@ def gem_destroy(g: int) -> None:
     _check(_L.gem_destroy(g), "gem_destroy")
 
 
+def gem_dims(g: int) -> tuple[int, int]:
+    """(P, n) of the handle."""
+    P, n = C.c_int64(), C.c_int32()
+    _check(_L.gem_dims(g, C.byref(P), C.byref(n)), "gem_dims")
+    return P.value, n.value
+
+
+def _host_f32(a, size: int, what: str) -> np.ndarray:
+    """A contiguous binary32 copy of a host array that must hold `size`
+    elements: the library reads or writes exactly that many."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    if a.size != size:
+        raise ValueError(f"{what}: {a.size} elements, the handle needs {size}")
+    return a
+
+
+def _same_size(g: int, P: int, what: str) -> None:
+    if P != gem_dims(g)[0]:
+        raise ValueError(f"{what}: P = {P}, the handle has P = {gem_dims(g)[0]}")
+
+
 def gem_set_theta(g: int, theta0, in_is_device: bool = False) -> None:
     if in_is_device:
         _check(_L.gem_set_theta(g, theta0, 1), "gem_set_theta")
     else:
-        a = np.ascontiguousarray(theta0, dtype=np.float32)
+        a = _host_f32(theta0, gem_dims(g)[0], "gem_set_theta")
         _check(_L.gem_set_theta(g, a.ctypes.data, 0), "gem_set_theta")
 
 
 def gem_set_quadratic(g: int, h, theta_star, sp: gem_sim_params) -> None:
-    h = np.ascontiguousarray(h, dtype=np.float32)
-    ts = np.ascontiguousarray(theta_star, dtype=np.float32)
+    P = gem_dims(g)[0]
+    h = _host_f32(h, P, "gem_set_quadratic (h)")
+    ts = _host_f32(theta_star, P, "gem_set_quadratic (theta_star)")
     _check(_L.gem_set_quadratic(g, h.ctypes.data, ts.ctypes.data, C.byref(sp)), "gem_set_quadratic")
 
 
@@ -232,18 +255,22 @@ def gem_sim_run(g: int, worker, tau, K: int) -> int:
 
 
 def gem_read_theta(g: int, P: int) -> np.ndarray:
+    _same_size(g, P, "gem_read_theta")
     out = np.empty(P, dtype=np.float32)
     _check(_L.gem_read_theta(g, out.ctypes.data, 0), "gem_read_theta")
     return out
 
 
 def gem_read_state(g: int, w: int, which: int, P: int) -> np.ndarray:
+    _same_size(g, P, "gem_read_state")
     out = np.empty(P, dtype=np.float32)
     _check(_L.gem_read_state(g, w, which, out.ctypes.data, 0), "gem_read_state")
     return out
 
 
 def gem_gather(g: int, idx, n: int):
+    if n != gem_dims(g)[1]:
+        raise ValueError(f"gem_gather: n = {n}, the handle has n = {gem_dims(g)[1]}")
     idx = np.ascontiguousarray(idx, dtype=np.int64)
     th = np.empty(idx.size, dtype=np.float32)
     S = np.empty((n, idx.size), dtype=np.float32)
@@ -260,6 +287,8 @@ def gem_clock(g: int) -> int:
 
 
 def gem_pull_clocks(g: int, n: int) -> np.ndarray:
+    if n != gem_dims(g)[1]:
+        raise ValueError(f"gem_pull_clocks: n = {n}, the handle has n = {gem_dims(g)[1]}")
     out = np.zeros(n, dtype=np.int64)
     _check(_L.gem_pull_clocks(g, _p(out, C.c_int64)), "gem_pull_clocks")
     return out

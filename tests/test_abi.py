@@ -100,6 +100,22 @@ def test_create_rejects_bad_arguments_before_device_work():
     hp.kappa_mode = G.GEM_KAPPA_SQRT
     hp.kappa = -1.0
     assert L.gem_create(16, 4, C.byref(hp), None, C.byref(out)) == G.GEM_EINVAL
+    # kappa scales a positive proxy energy (appendix B), in either form
+    for mode in (G.GEM_KAPPA_LINEAR, G.GEM_KAPPA_SQRT):
+        for kappa in (0.0, -0.0, -2.0, float("nan")):
+            hp = G.gem_hyperparams_default()
+            hp.kappa_mode = mode
+            hp.kappa = kappa
+            assert L.gem_create(16, 4, C.byref(hp), None, C.byref(out)) == G.GEM_EINVAL
+    # eps keeps |dtheta| + eps away from zero (Alg. 1): with eps = 0 an update
+    # of exactly zero would give pi = inf and theta = inf * 0 = NaN
+    for eps in (0.0, -0.0, -1e-16, float("inf"), float("nan")):
+        hp = G.gem_hyperparams_default()
+        hp.eps = eps
+        assert L.gem_create(16, 4, C.byref(hp), None, C.byref(out)) == G.GEM_EINVAL
+    hp = G.gem_hyperparams_default()
+    hp.eps = 1e-45                       # the smallest positive binary32 is accepted
+    assert hp.eps > 0
     # sizes: P above the largest grid, and a table whose byte count wraps 64 bits
     assert L.gem_create(G.GEM_P_MAX + 1, 1, None, None, C.byref(out)) == G.GEM_EINVAL
     assert L.gem_create(G.GEM_P_MAX, 2**31 - 1, None, None, C.byref(out)) == G.GEM_ENOMEM
@@ -119,6 +135,8 @@ def test_null_handle_calls_fail_cleanly():
     assert L.gem_commit(None, None, 0) == G.GEM_EINVAL
     assert L.gem_sim_run(None, None, None, 0, 1) == G.GEM_EINVAL
     assert L.gem_copy_f32(None, None, 4, None) == G.GEM_EINVAL
+    P, n = C.c_int64(), C.c_int32()
+    assert L.gem_dims(None, C.byref(P), C.byref(n)) == G.GEM_EINVAL
 
 
 def test_one_hip_runtime_per_process():
