@@ -204,9 +204,61 @@ def test_rejected_calls_change_nothing(env):
         idx = np.zeros(4, np.int64)
         assert L.gem_gather(g.h, idx.ctypes.data_as(C.POINTER(C.c_int64)), G.GEM_P_MAX + 1,
                             None, None, None) == G.GEM_EINVAL
+        # host buffers of the wrong length are refused by the binding before
+        # the library could read or write past their ends
+        assert G.gem_dims(g.h) == (P, n)
+        with pytest.raises(ValueError):
+            G.gem_set_quadratic(g.h, np.ones(P - 1, np.float32), np.zeros(P, np.float32),
+                                G.gem_sim_params(lr=0.01))
+        with pytest.raises(ValueError):
+            G.gem_set_theta(g.h, np.zeros(P - 3, np.float32))
+        with pytest.raises(ValueError):
+            G.gem_read_theta(g.h, P + 1)
+        with pytest.raises(ValueError):
+            G.gem_read_state(g.h, 0, G.GEM_SNAPSHOT, P - 1)
+        with pytest.raises(ValueError):
+            G.gem_gather(g.h, [0, 1], n + 1)
+        with pytest.raises(ValueError):
+            G.gem_pull_clocks(g.h, n - 1)
         after = (g.theta(), g.S(), g.M(), g.clock, g.pull_clocks())
     for x, y in zip(before, after):
         assert np.array_equal(x, y)
+
+
+def test_hyperparameters_out_of_range_are_refused(env):
+    """eps <= 0 would let an update of exactly zero divide zero by zero in
+    pi's denominator (Alg. 1) and turn theta into NaN; kappa scales a positive
+    proxy energy.  Both are refused at create and in a checkpoint header."""
+    torch, G = env
+    for field, value in (("eps", 0.0), ("eps", -1e-16), ("kappa", 0.0), ("kappa", -1.0)):
+        hp = G.gem_hyperparams_default()
+        setattr(hp, field, value)
+        with pytest.raises(G.GemError) as e:
+            G.Gem(64, 2, hp)
+        assert e.value.code == G.GEM_EINVAL
+    # the smallest positive eps still keeps an update of exactly zero from moving theta
+    hp = G.gem_hyperparams_default()
+    hp.eps = 1e-45
+    d = torch.zeros(64, dtype=torch.float32, device="cuda")
+    with G.Gem(64, 2, hp) as g:
+        g.commit(d.data_ptr(), 1)
+        g.commit(d.data_ptr(), 0)
+        assert np.all(g.theta() == 0) and np.all(np.isfinite(g.M()))
+
+
+def test_load_refuses_a_header_with_eps_zero(env, tmp_path):
+    torch, G = env
+    path = str(tmp_path / "ck.bin")
+    with G.Gem(64, 2) as g:
+        assert G.gem_save(g.h, path) == G.GEM_OK
+        raw = bytearray(open(path, "rb").read())
+        # header: magic[8], P int64, n int32, have_problem int32, t int64, then
+        # the hyper-parameters (momentum, eps, kappa as binary32 first)
+        eps_at = 8 + 8 + 4 + 4 + 8 + 4
+        assert np.frombuffer(bytes(raw[eps_at:eps_at + 4]), np.float32)[0] == np.float32(1e-16)
+        raw[eps_at:eps_at + 4] = np.float32(0.0).tobytes()
+        open(path, "wb").write(bytes(raw))
+        assert G.gem_load(g.h, path) == G.GEM_EIO
 
 
 def test_empty_batch_and_run_are_no_ops(env):

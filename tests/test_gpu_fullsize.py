@@ -1,11 +1,14 @@
 """Parity at the workloads' full sizes, in the launch configuration the
 benchmark times (gem_sim_run over the whole schedule with the workload's K).
 
-The GPU runs every element; the oracle runs a sample of element indices (the
-first and last chunks, the ragged tail and random indices).  Each element's
-trajectory depends only on its own inputs, the schedule and the seed, so the
-oracle's subset run equals those entries of a full run (pinned on the CPU by
-test_subset_run_equals_full_run)."""
+The GPU runs every element; the oracle runs a sample of element indices: one
+index in every block of 1024 elements (the elements one 256-thread block of
+the pass owns, whose tile base and row offsets are block-uniform), at a lane
+position that rotates through all 1024 positions, both sides of every
+8192-element table-tile edge, the first and last chunks, the ragged tail and
+random indices.  Each element's trajectory depends only on its own inputs,
+the schedule and the seed, so the oracle's subset run equals those entries of
+a full run (pinned on the CPU by test_subset_run_equals_full_run)."""
 import numpy as np
 import pytest
 
@@ -24,13 +27,22 @@ def G():
     return gem
 
 
+BLOCK_ELEMS = 1024    # elements of one pass-kernel block (256 threads x 4)
+TILE_ELEMS = 8192     # elements of one table tile
+
+
 def _sample(P, k=2048, seed=0):
     rng = np.random.default_rng(seed)
     fixed = np.array([0, 1, 2, 3, 4, 5, 6, 7, P // 2, P - 8, P - 7, P - 6, P - 5, P - 4, P - 3,
                       P - 2, P - 1])
-    idx = np.unique(np.concatenate([fixed[(fixed >= 0) & (fixed < P)],
-                                    rng.integers(0, P, size=k)]))
-    return idx.astype(np.int64)
+    # one index per block; 389 is odd, so the offsets run through every lane
+    # position (and every element of a 16-byte chunk) once per 1024 blocks
+    blocks = np.arange(-(-P // BLOCK_ELEMS), dtype=np.int64)
+    per_block = blocks * BLOCK_ELEMS + (blocks * 389) % BLOCK_ELEMS
+    edges = np.arange(1, -(-P // TILE_ELEMS), dtype=np.int64) * TILE_ELEMS
+    idx = np.concatenate([fixed, per_block, edges - 1, edges, rng.integers(0, P, size=k)])
+    return np.unique(idx[(idx >= 0) & (idx < P)]).astype(np.int64)
+
 
 
 def _free_bytes():
