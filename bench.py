@@ -28,14 +28,25 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# VALU issue ceiling of one MI355X: the fp32 vector peak, 157.3 TFLOP/s =
+# 256 CUs x 2.4 GHz x 256 flop per CU and cycle, is two wave64 FMA
+# instructions (128 flop each) per CU and cycle: 1228.8 G wave64 VALU
+# instructions per second.  Instructions slower than a full-rate FMA (64-bit
+# integer multiplies, transcendental approximations) only lower what a real
+# instruction mix can reach.
+VALU_PEAK_GINST = 256 * 2.4 * 2
 METRIC = "parameter-commits/s (P×commits/s) + achieved HBM GB/s vs peak, P=25M n=100"
 KERNEL_SOURCES = ("gem_kernels.hip", "gem_device.hpp", "gem_internal.hpp", "gem_plan.hpp",
                   "gem_layout.hpp")
-# Committed rocprofv3 counter summaries, per (workload, proxy) of the fast kernel variants.
+# Committed rocprofv3 counter summaries of the dominant kernel, per (workload,
+# proxy, pi scope), each taken with the library's own cache rule.
 COUNTERS_FILES = {
-    ("headline", "local"): os.path.join(ROOT, "profiles", "pass_kernel_headline_counters.md"),
-    ("headline", "global"): os.path.join(ROOT, "profiles",
-                                         "pass_kernel_headline_global_proxy_counters.md"),
+    ("headline", "local", "element"): "pass_kernel_headline_counters.md",
+    ("headline", "global", "element"): "pass_kernel_headline_global_proxy_counters.md",
+    ("small", "local", "element"): "pass_kernel_small_counters.md",
+    ("resnet18", "local", "element"): "pass_kernel_resnet18_counters.md",
+    ("large", "local", "element"): "pass_kernel_large_counters.md",
+    ("headline", "local", "segment"): "seg_step_kernel_headline_counters.md",
 }
 
 
@@ -53,10 +64,12 @@ def kernel_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str, proxy: str):
-    """HBM bytes per pass from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source for this workload; else None."""
-    path = COUNTERS_FILES.get((workload, proxy))
+def measured_counters(workload: str, proxy: str, scope: str):
+    """The machine-readable block of the committed rocprofv3 counter summary
+    for this configuration (HBM bytes and VALU instructions per launch of the
+    dominant kernel), if it was taken on the current kernel source; else None."""
+    name = COUNTERS_FILES.get((workload, proxy, scope))
+    path = os.path.join(ROOT, "profiles", name) if name else None
     if path is None or not os.path.exists(path):
         return None
     text = open(path).read()
@@ -65,9 +78,27 @@ def measured_traffic(workload: str, proxy: str):
         return None
     d = json.loads(m.group(1))
     if (d.get("kernel_hash") != kernel_hash() or d.get("workload") != workload
-            or d.get("proxy", "local") != proxy):
+            or d.get("proxy", "local") != proxy or d.get("pi_scope", "element") != scope):
         return None
-    return d.get("hbm_bytes_per_pass")
+    return d
+
+
+def host_description() -> dict:
+    """The CPU the oracle baseline ran on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = None
+    return {"cpu_model": model, "logical_cores": os.cpu_count(), "usable_cores": usable}
 
 
 def cpu_baseline(wl, h, ts, worker, tau, sample_elems: int, sample_commits: int, ghp):
@@ -91,6 +122,7 @@ def cpu_baseline(wl, h, ts, worker, tau, sample_elems: int, sample_commits: int,
         "kind": "oracle",
         "sample": f"first {sample_commits} commits of the {wl.name} schedule on parameters "
                   f"0..{sample_elems - 1} ({dt:.1f} s, single thread)",
+        "host": host_description(),
     }
 
 
@@ -111,6 +143,45 @@ def copy_ceiling(G, torch, nbytes: int, reps: int = 10) -> float:
     ms = e0.elapsed_time(e1) / reps
     del src, dst
     return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def compute_floor(G, torch, wl, hp, cache: int, pi_hist: bool, passes: int = 12) -> float:
+    """Milliseconds of compute per commit of the workload's pass kernel: the
+    same kernel over the same P with one worker, in passes of GEM_K_MAX
+    commits.  That worker's snapshot and moment stay in the register slots for
+    the whole pass, so a pass moves 32 bytes per parameter for 32 commits and
+    its time is the noise generator's and the commit arithmetic's.  A real
+    configuration of the method (GEM with a single worker), run through
+    gem_sim_run."""
+    import numpy as np
+    stream = torch.cuda.current_stream()
+    K = G.GEM_K_MAX
+    T = passes * K
+    worker = np.zeros(T, dtype=np.int32)
+    with G.Gem(wl.P, 1, hp, stream=stream.cuda_stream) as g:
+        g.set_cache_policy(cache)
+        g.set_quadratic(*problem_arrays(wl), wl.lr, wl.sigma, wl.seed, bf16=wl.bf16)
+        g.sim_run(worker[:2 * K], None, K)                  # warm-up
+        if pi_hist:
+            G.gem_pi_hist_start(g.h, T)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.sim_run(worker, None, K)
+        e1.record(stream)
+        torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / T
+
+
+_PROBLEM = {}
+
+
+def problem_arrays(wl):
+    """h and theta* of the workload (drawn once per process)."""
+    from paper_1805_08469_amd.workloads import problem
+    if wl.name not in _PROBLEM:
+        _PROBLEM[wl.name] = problem(wl)
+    return _PROBLEM[wl.name]
 
 
 def compare_rules(G, P: int = 1 << 20, T: int = 3000, every: int = 500, K: int = 16):
@@ -216,7 +287,7 @@ def main() -> int:
         return 0
 
     wl = WORKLOADS[args.workload]
-    h, ts = problem(wl)
+    h, ts = problem_arrays(wl)
     total = (args.warmup + args.steps) * wl.T
     worker, tau = G.gem_schedule_make(wl.n, total, wl.law, wl.law_p0, wl.law_p1, seed=wl.seed)
 
@@ -239,9 +310,10 @@ def main() -> int:
     streaming = state_bytes > (256 << 20) if args.cache == "auto" else args.cache == "stream"
 
     stream = torch.cuda.current_stream()
+    cache = {"auto": G.GEM_CACHE_AUTO, "keep": G.GEM_CACHE_KEEP,
+             "stream": G.GEM_CACHE_STREAM}[args.cache]
     g = G.Gem(wl.P, wl.n, hp, stream=stream.cuda_stream)
-    g.set_cache_policy({"auto": G.GEM_CACHE_AUTO, "keep": G.GEM_CACHE_KEEP,
-                        "stream": G.GEM_CACHE_STREAM}[args.cache])
+    g.set_cache_policy(cache)
     g.set_quadratic(h, ts, wl.lr, wl.sigma, wl.seed, bf16=wl.bf16)
     torch.cuda.synchronize()
 
@@ -273,6 +345,10 @@ def main() -> int:
     assert stats.commits == args.steps * wl.T
     g.close()
     copy_gbs = copy_ceiling(G, torch, 2 << 30)
+    # The compute floor of a pass of K commits (not defined for the
+    # per-segment scope, whose commits are not fused).
+    floor_ms = (compute_floor(G, torch, wl, hp, cache, args.pi_hist) * wl.K
+                if args.pi_scope == "element" else None)
 
     elapsed = max(gpu_s, 1e-12)
     value = wl.P * stats.commits / elapsed
@@ -281,8 +357,24 @@ def main() -> int:
     avg_pass_s = elapsed / passes
     achieved = alg_per_pass / avg_pass_s / 1e9
     # The counter summaries were taken with the library's own cache rule.
-    traffic = (measured_traffic(wl.name, args.proxy)
-               if fast and args.cache == "auto" and not args.pi_hist else None)
+    counted = (args.rule, args.pi, args.kappa) == ("gem", "clamp0", 1.0)
+    cnt = (measured_counters(wl.name, args.proxy, args.pi_scope)
+           if counted and args.cache == "auto" and not args.pi_hist else None)
+    traffic = cnt.get("hbm_bytes_per_pass") if cnt else None
+    floor_share = floor_ms / (avg_pass_s * 1e3) if floor_ms else None
+    # The pass is reported against the ceiling it is nearer to: the compute
+    # floor of its arithmetic, or the library's copy rate on HBM.
+    if floor_share is not None and floor_share > achieved / copy_gbs:
+        valu = cnt.get("valu_instrs_per_pass") if cnt else None
+        ach = valu / avg_pass_s / 1e9 if valu else None
+        roof = {"bound": "alu", "achieved": ach, "peak": VALU_PEAK_GINST,
+                "unit": "G wave64 VALU instructions/s",
+                "frac": ach / VALU_PEAK_GINST if ach else None, "traffic": traffic,
+                "valu_instrs_per_launch": valu,
+                "hbm_GBps": achieved, "hbm_frac": achieved / HBM_PEAK_GBS}
+    else:
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS, "traffic": traffic}
 
     result = {
         "metric": METRIC,
@@ -310,12 +402,7 @@ def main() -> int:
             "parallelism": "single-gpu",
         },
         "roofline": {
-            "bound": "hbm",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
-            "traffic": traffic,
+            **roof,
             "alg_bytes_per_launch": alg_per_pass,
             "avg_launch_ms": avg_pass_s * 1e3,
             "kernel": (("seg_step_kernel + seg_blocks_kernel" + (", streaming" if streaming else ""))
@@ -327,6 +414,8 @@ def main() -> int:
                        % (variant, depth, ", streaming" if streaming else "")),
             "copy_ceiling_GBps": copy_gbs,
             "frac_of_copy": achieved / copy_gbs,
+            "compute_floor_ms": floor_ms,
+            "frac_of_compute_floor": floor_share,
         },
         "wall_s": wall,
     }
