@@ -25,6 +25,18 @@ struct Words4 {
     uint32_t x0, x1, x2, x3;
 };
 
+// a ^ b ^ c.  On the device one V_BITOP3_B32 (gfx950's three-input bitwise
+// operation; truth table 0x96 is the odd-parity function), which the compiler
+// does not form from two XORs by itself.
+__host__ __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c)
+{
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+#else
+    return a ^ b ^ c;
+#endif
+}
+
 __host__ __device__ __forceinline__ Words4 philox10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
                                           uint32_t k0, uint32_t k1)
 {
@@ -32,8 +44,8 @@ __host__ __device__ __forceinline__ Words4 philox10(uint32_t c0, uint32_t c1, ui
     for (int r = 0; r < 10; ++r) {
         const uint64_t pa = static_cast<uint64_t>(0xD2511F53u) * c0;
         const uint64_t pb = static_cast<uint64_t>(0xCD9E8D57u) * c2;
-        const uint32_t y0 = static_cast<uint32_t>(pb >> 32) ^ c1 ^ k0;
-        const uint32_t y2 = static_cast<uint32_t>(pa >> 32) ^ c3 ^ k1;
+        const uint32_t y0 = xor3(static_cast<uint32_t>(pb >> 32), c1, k0);
+        const uint32_t y2 = xor3(static_cast<uint32_t>(pa >> 32), c3, k1);
         c1 = static_cast<uint32_t>(pb);
         c3 = static_cast<uint32_t>(pa);
         c0 = y0;
@@ -97,6 +109,21 @@ __device__ __forceinline__ float div_rn(float num, float den)
     return q;
 }
 
+// (f - 1) / (f + 1), correctly rounded, for the binary32 f in (sqrt(1/2),
+// sqrt(2)] the logarithm below reduces to: the hardware reciprocal r of
+// f + 1 and one residual correction of the quotient (f - 1) r.  f - 1 is exact,
+// f + 1 lies in (1.7, 2.5), and on these 2^23 operand pairs the two steps
+// give the correctly rounded quotient every time (the self-test library
+// checks all of them on the device against the IEEE division); the general
+// core above takes four more steps.
+__device__ __forceinline__ float ln_quotient(float a, float b)
+{
+    const float r = __builtin_amdgcn_rcpf(b);
+    const float q = a * r;
+    const float e = __builtin_fmaf(-b, q, a);
+    return __builtin_fmaf(e, r, q);
+}
+
 // ---------------------------------------------------------------------------
 // Natural logarithm of u = k * 2^-24 for an integer k in [1, 2^24] (the Box-
 // Muller radius argument).  u = 2^e f with f in (sqrt(1/2), sqrt(2)];
@@ -104,18 +131,18 @@ __device__ __forceinline__ float div_rn(float num, float den)
 // Stegun 4.1.27); ln u = e ln2 + ln f with ln 2 split into a 15-bit head and
 // a binary32 tail so that e * head is exact.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float ln_of_unit(float u)
+
+// ln of the positive normal binary32 value with bit pattern `bits`, scaled by
+// 2^(127 - bias): bias 127 gives ln of the value itself.
+__device__ __forceinline__ float ln_from_bits(uint32_t bits, int bias)
 {
-    const uint32_t bits = __float_as_uint(u);
-    int e = static_cast<int>(bits >> 23) - 127;   // u > 0, so the sign bit is clear
+    int e = static_cast<int>(bits >> 23) - bias;  // positive: the sign bit is clear
     const uint32_t mant = bits & 0x007FFFFFu;
     const bool upper = mant > 0x003504F3u;        // 1.mant above sqrt(2) in binary32
     const uint32_t fbits = mant | (upper ? 0x3F000000u : 0x3F800000u);
     e += upper ? 1 : 0;
     const float f = __uint_as_float(fbits);
-    // f - 1 is exact and 0 or at least 2^-24 in magnitude, f + 1 in (1.7, 2.5):
-    // the division needs no scaling.
-    const float s = div_rn_core(f - 1.0f, f + 1.0f);
+    const float s = ln_quotient(f - 1.0f, f + 1.0f);
     const float z = s * s;
     float p = 1.0f / 9.0f;
     p = __builtin_fmaf(p, z, 1.0f / 7.0f);
@@ -130,6 +157,17 @@ __device__ __forceinline__ float ln_of_unit(float u)
     float r = __builtin_fmaf(ef, ln2_tail, ln_f);
     r = __builtin_fmaf(ef, ln2_head, r);
     return r;
+}
+
+// ln u for u = k 2^-24 in (0, 1].
+__device__ __forceinline__ float ln_of_unit(float u) { return ln_from_bits(__float_as_uint(u), 127); }
+
+// The same from k: the binary32 k (exact) has the significand of u and an
+// exponent 24 larger, so the scaling by 2^-24 folds into the exponent's bias
+// instead of a multiplication.
+__device__ __forceinline__ float ln_of_k24(uint32_t k)
+{
+    return ln_from_bits(__float_as_uint(static_cast<float>(k)), 127 + 24);
 }
 
 // sin and cos of 2 pi k / 2^24, k in [0, 2^24).  The angle is reduced to the
@@ -168,9 +206,8 @@ __device__ __forceinline__ void sincos_of_turn(uint32_t k, float& sn, float& cs)
 // the angle index xb >> 8, the pair r cos(phi), r sin(phi), r = sqrt(-2 ln u1).
 __device__ __forceinline__ void box_muller(uint32_t xa, uint32_t xb, float& zc, float& zs)
 {
-    const float u1 = static_cast<float>((xa >> 8) + 1u) * 0x1p-24f;
     // -2 ln u1 is +0 (u1 = 1) or at least 1.1e-7: no scaling.
-    const float r = sqrt_rn_core(-2.0f * ln_of_unit(u1));
+    const float r = sqrt_rn_core(-2.0f * ln_of_k24((xa >> 8) + 1u));
     float sn, cs;
     sincos_of_turn(xb >> 8, sn, cs);
     zc = r * cs;

@@ -433,7 +433,13 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
         __syncthreads();
     }
     if (global_m) ch.mg = r.out.m;
-    if (dst != kToMemory) held = held_put(held, dst, r.out);
+    if (dst != kToMemory) {
+        // The shared-moment variant carries the moment in ch.mg: a held
+        // slot keeps only the snapshot (no registers for a moment copy).
+        Rows keep = r.out;
+        if (V == Variant::FastGlobal) keep.m = make_float4(0.f, 0.f, 0.f, 0.f);
+        held = held_put(held, dst, keep);
+    }
     r.held = held;
     if (ch.active) {
         // With the shared moment, only snapshot rows move; moment traffic goes

@@ -4,7 +4,8 @@
 // The commit kernels use range-specialised forms of correctly rounded
 // division and square root (gem_device.hpp).  These kernels compare them, on
 // the device and bit for bit, with hipcc's general IEEE operations:
-//   - the logarithm's (f - 1) / (f + 1) for every binary32 f the logarithm
+//   - the logarithm's (f - 1) / (f + 1) (ln_quotient, and the general core
+//     div_rn_core on the same operands) for every binary32 f the logarithm
 //     can see (the 2^23 values in (sqrt(1/2), sqrt(2)]);
 //   - the Box-Muller radius sqrt(-2 ln u) for every u = k 2^-24, k in
 //     [1, 2^24];
@@ -40,7 +41,10 @@ __global__ __launch_bounds__(kThreads) void ln_div_kernel(unsigned long long* ba
     if (upper != (mant > 0x003504F3u)) return;   // the logarithm picks the branch by mant
     const float f = __uint_as_float(mant | (upper ? 0x3F000000u : 0x3F800000u));
     const float a = f - 1.0f, b = f + 1.0f;
-    if (!same_bits(gemk::div_rn_core(a, b), a / b)) atomicAdd(bad, 1ull);
+    const float want = a / b;
+    // the two forms the library uses for this quotient
+    if (!same_bits(gemk::ln_quotient(a, b), want)) atomicAdd(bad, 1ull);
+    if (!same_bits(gemk::div_rn_core(a, b), want)) atomicAdd(bad, 1ull);
 }
 
 __global__ __launch_bounds__(kThreads) void radius_kernel(unsigned long long* bad)
@@ -49,6 +53,9 @@ __global__ __launch_bounds__(kThreads) void radius_kernel(unsigned long long* ba
     const float u = static_cast<float>(k) * 0x1p-24f;
     const float x = -2.0f * gemk::ln_of_unit(u);
     if (!same_bits(gemk::sqrt_rn_core(x), __builtin_sqrtf(x))) atomicAdd(bad, 1ull);
+    // the two ways to the logarithm (from u, and from k with the scaling in
+    // the exponent) agree
+    if (!same_bits(gemk::ln_of_k24(k), gemk::ln_of_unit(u))) atomicAdd(bad, 1ull);
 }
 
 // A binary32 value from 32 random bits, with the exponent field drawn over
