@@ -50,6 +50,7 @@ extern "C" {
 #define GEM_ESTATE   (-7)  /* the call needs set-up that has not happened (no problem set) */
 #define GEM_EIO      (-8)  /* checkpoint file could not be read or written, or does not match */
 #define GEM_EALIGN   (-9)  /* a device buffer is not aligned as required */
+#define GEM_ESCRATCH (-10) /* the request does not fit the fixed device scratch */
 
 /* ---- enums --------------------------------------------------------------- */
 enum { GEM_F32 = 0, GEM_BF16 = 1 };                        /* update element type */
@@ -242,6 +243,23 @@ int gem_read_state(gem_t* g, int32_t w, int32_t which, float* out, int32_t out_i
  * GEM_P_MAX (EINVAL above).  ENOMEM if the device staging cannot be allocated. */
 int gem_gather(gem_t* g, const int64_t* idx, int64_t count, float* theta_out, float* S_out,
                float* M_out);
+
+/* gem_gather for callers that cannot allocate memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid allocation): the same outputs,
+ * bit for bit, staged through a fixed device scratch of GEM_SCRATCH_BYTES
+ * that the library holds on each GPU it runs on until the process ends,
+ * instead of buffers allocated per call.  The call allocates nothing, on the
+ * device or the host.  The indices and the gathered values must fit the
+ * scratch: count * (8 + 4 * (1 + 2 n)) <= GEM_SCRATCH_BYTES, else
+ * GEM_ESCRATCH and nothing is done (count <= 5165 at n = 100).  Other errors
+ * as gem_gather.  All handles on one GPU share its scratch: calls that
+ * overlap on one GPU (handles used from several threads, or on streams that
+ * run concurrently) race and must be serialised by the caller.  The scratch
+ * keeps the last call's contents; nothing in it needs to start at zero.
+ * Synchronises the handle's stream. */
+#define GEM_SCRATCH_BYTES (4 << 20)
+int gem_gather_static(gem_t* g, const int64_t* idx, int64_t count, float* theta_out,
+                      float* S_out, float* M_out);
 
 /* The handle's sizes: P parameters and n workers (what every host buffer of
  * P or n elements passed to or filled by the calls here must hold).

@@ -65,6 +65,7 @@ struct gem_handle {
     uint32_t deep_lds = 0;           // LDS reserved per block of the deep-ring pass
     int64_t npart = 0;
     int64_t nsup = 0;
+    void* scratch = nullptr;         // this device's static scratch (gem_gather_static)
 };
 
 namespace {
@@ -492,6 +493,7 @@ const char* gem_strerror(int code)
     case GEM_ESTATE: return "operation needs a problem set with gem_set_quadratic";
     case GEM_EIO: return "checkpoint I/O error or mismatch";
     case GEM_EALIGN: return "device buffer not aligned";
+    case GEM_ESCRATCH: return "request does not fit the fixed device scratch";
     default: return "unknown error";
     }
 }
@@ -551,6 +553,16 @@ int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, ge
         const hipError_t e = hipGetDevice(&g->device);
         if (e != hipSuccess) {
             note_hip_error("hipGetDevice", e, __LINE__);
+            delete g;
+            return GEM_EHIP;
+        }
+    }
+    {
+        // The static scratch of the allocation-free entry point: its device
+        // address on this (current) device, looked up once per device.
+        const hipError_t e = gemk::scratch_address(g->device, &g->scratch);
+        if (e != hipSuccess) {
+            note_hip_error("hipGetSymbolAddress(scratch)", e, __LINE__);
             delete g;
             return GEM_EHIP;
         }
@@ -798,6 +810,41 @@ int gem_gather(gem_t* g, const int64_t* idx, int64_t count, float* theta_out, fl
     (void)hipFree(d_idx);
     (void)hipFree(d_out);
     return rc;
+}
+
+int gem_gather_static(gem_t* g, const int64_t* idx, int64_t count, float* theta_out,
+                      float* S_out, float* M_out)
+{
+    if (!g || count < 0 || (count > 0 && !idx)) return GEM_EINVAL;
+    if (count == 0) return GEM_OK;
+    const int64_t rows = 1 + 2 * static_cast<int64_t>(g->n);
+    const int64_t per_index = 8 + 4 * rows;   // the index and its gathered values
+    if (count > GEM_SCRATCH_BYTES / per_index) return GEM_ESCRATCH;
+    for (int64_t k = 0; k < count; ++k)
+        if (idx[k] < 0 || idx[k] >= g->P) return GEM_EINVAL;
+    // Scratch layout: the indices, then theta, then the S rows, then the M
+    // rows of the gathered entries (the byte counts keep each part 4-aligned
+    // and the indices 8-aligned at the 256-byte aligned start).
+    auto* d_idx = static_cast<int64_t*>(g->scratch);
+    float* d_out = reinterpret_cast<float*>(d_idx + count);
+    GEM_HIP(hipMemcpyAsync(d_idx, idx, static_cast<size_t>(count) * sizeof(int64_t),
+                           hipMemcpyHostToDevice, g->stream));
+    if (theta_out) GEM_HIP(gemk::launch_gather(g->theta, d_idx, count, d_out, g->stream));
+    if (S_out) GEM_HIP(gemk::launch_gather_rows(g->S, g->n, d_idx, count, d_out + count, g->stream));
+    if (M_out)
+        GEM_HIP(gemk::launch_gather_rows(g->M, g->n, d_idx, count, d_out + (1 + g->n) * count,
+                                         g->stream));
+    const size_t row_bytes = static_cast<size_t>(count) * sizeof(float);
+    if (theta_out)
+        GEM_HIP(hipMemcpyAsync(theta_out, d_out, row_bytes, hipMemcpyDeviceToHost, g->stream));
+    if (S_out)
+        GEM_HIP(hipMemcpyAsync(S_out, d_out + count, row_bytes * g->n, hipMemcpyDeviceToHost,
+                               g->stream));
+    if (M_out)
+        GEM_HIP(hipMemcpyAsync(M_out, d_out + (1 + g->n) * count, row_bytes * g->n,
+                               hipMemcpyDeviceToHost, g->stream));
+    GEM_HIP(hipStreamSynchronize(g->stream));
+    return GEM_OK;
 }
 
 int gem_dims(gem_t* g, int64_t* P, int32_t* n)

@@ -164,6 +164,10 @@ hipError_t launch_gather_rows(const float* base, int64_t nw, const int64_t* idx,
                               float* out, hipStream_t stream);
 hipError_t launch_loss(const float* theta, const float* h, const float* ts, int64_t P,
                        double* out, hipStream_t stream);
+// Device address of the current GPU's copy of the library's static scratch
+// (GEM_SCRATCH_BYTES, 256-byte aligned); device is the current device.  The
+// address is looked up once per device and kept.
+hipError_t scratch_address(int device, void** out);
 hipError_t launch_copy(const float* src, float* dst, int64_t count, hipStream_t stream);
 
 }  // namespace gemk

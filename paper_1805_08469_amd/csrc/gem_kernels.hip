@@ -17,10 +17,40 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "gem_device.hpp"
 #include "gem_internal.hpp"
 
+// Device scratch of the allocation-free entry point (gem_gather_static): one
+// copy per GPU, held until the process ends.  In host code this name is only a
+// stand-in for the symbol; the device address of the current GPU's copy comes
+// from hipGetSymbolAddress (scratch_address below), and only that address is
+// ever passed to kernels or copies.
+static __device__ __align__(256) unsigned char scratch[GEM_SCRATCH_BYTES];
+
 namespace gemk {
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+}  // namespace
+
+hipError_t scratch_address(int device, void** out)
+{
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[device]) {
+        // once per device, with that device current (the caller's)
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_dev[device] = p;
+    }
+    *out = g_scratch_dev[device];
+    return hipSuccess;
+}
 
 namespace {
 

@@ -24,6 +24,8 @@ LIB_PATH = os.environ.get("LIBGEM_PATH") or os.path.join(_HERE, "libgem.so")
 
 GEM_OK, GEM_EINVAL, GEM_ENOMEM, GEM_EWORKER, GEM_ESTALE = 0, -1, -2, -3, -4
 GEM_EDTYPE, GEM_EHIP, GEM_ESTATE, GEM_EIO, GEM_EALIGN = -5, -6, -7, -8, -9
+GEM_ESCRATCH = -10
+GEM_SCRATCH_BYTES = 4 << 20
 GEM_F32, GEM_BF16 = 0, 1
 GEM_PI_CLAMP0, GEM_PI_LITERAL = 0, 1
 GEM_KAPPA_LINEAR, GEM_KAPPA_SQRT = 0, 1
@@ -46,7 +48,7 @@ EXPORTED = (
     "gem_pull_clocks", "gem_reset_worker", "gem_diag_enable", "gem_diag_reset", "gem_diag",
     "gem_stats", "gem_stats_reset", "gem_save", "gem_load", "gem_sync", "gem_copy_f32",
     "gem_pi_hist_start", "gem_pi_hist_start_segments", "gem_pi_hist_read", "gem_set_segments",
-    "gem_set_cache_policy", "gem_dims",
+    "gem_set_cache_policy", "gem_dims", "gem_gather_static",
 )
 
 
@@ -114,6 +116,7 @@ def _load():
         "gem_read_theta": (C.c_int, [vp, vp, C.c_int32]),
         "gem_read_state": (C.c_int, [vp, C.c_int32, C.c_int32, vp, C.c_int32]),
         "gem_gather": (C.c_int, [vp, i64p, C.c_int64, vp, vp, vp]),
+        "gem_gather_static": (C.c_int, [vp, i64p, C.c_int64, vp, vp, vp]),
         "gem_clock": (C.c_int, [vp, i64p]),
         "gem_dims": (C.c_int, [vp, i64p, i32p]),
         "gem_pull_clocks": (C.c_int, [vp, i64p]),
@@ -277,6 +280,21 @@ def gem_gather(g: int, idx, n: int):
     M = np.empty((n, idx.size), dtype=np.float32)
     _check(_L.gem_gather(g, _p(idx, C.c_int64), idx.size, th.ctypes.data, S.ctypes.data,
                          M.ctypes.data), "gem_gather")
+    return th, S, M
+
+
+def gem_gather_static(g: int, idx, n: int):
+    """gem_gather through the library's fixed device scratch (no allocation
+    in the library); raises GemError(GEM_ESCRATCH) for a request that does
+    not fit it."""
+    if n != gem_dims(g)[1]:
+        raise ValueError(f"gem_gather_static: n = {n}, the handle has n = {gem_dims(g)[1]}")
+    idx = np.ascontiguousarray(idx, dtype=np.int64)
+    th = np.empty(idx.size, dtype=np.float32)
+    S = np.empty((n, idx.size), dtype=np.float32)
+    M = np.empty((n, idx.size), dtype=np.float32)
+    _check(_L.gem_gather_static(g, _p(idx, C.c_int64), idx.size, th.ctypes.data, S.ctypes.data,
+                                M.ctypes.data), "gem_gather_static")
     return th, S, M
 
 

@@ -46,7 +46,7 @@ def test_defaults_are_alg1():
 
 
 def test_strerror_covers_codes():
-    for code in range(0, -10, -1):
+    for code in range(0, -11, -1):
         assert G.gem_strerror(code) != "unknown error"
     assert G.gem_strerror(-99) == "unknown error"
 
