@@ -302,7 +302,7 @@ int gem_diag(gem_t* g, gem_diag_t* out);
  * added by the adjacent-pairs tree, then the blocks in increasing order), the
  * norm is its binary64 square root rounded to binary32, and pi_T follows in
  * binary32; segments of one element give element-wise GEM bit for bit.
- * Each commit is one streaming launch plus two small reduction launches (a
+ * Each commit is one streaming launch plus one small reduction launch (a
  * commit's pi needs every element of its segment first), so commits are not
  * fused.  pi histograms record each segment's factor once per element (one
  * bin per segment holding its size); the diagnostics count the elements of
@@ -342,9 +342,13 @@ int gem_pi_hist_read(gem_t* g, uint32_t* out, int64_t max_commits, int64_t* comm
  * worker's S and M rows read and written once (GLOBAL proxy: its S row, plus
  * the shared moment read and written once), and caller updates read -- 4
  * bytes per float, 2 per bfloat16.  Under GEM_PI_SEGMENT every commit is one
- * pass and counts 36 bytes per element (generated updates: theta, the
- * committing and the pending worker's snapshot, the pull, M, h and theta*)
- * or 32 / 28 (given f32 / bf16 updates, each read twice). */
+ * pass and counts 32 bytes per element (generated updates: theta read, the
+ * committing and the pending worker's snapshot read, the pull written, M
+ * read and written, h and theta* read) or 28 / 24 (given f32 / bf16 updates,
+ * each read twice); with GEM_PULL_PRE_COMMIT theta is also written (4 more).
+ * With post-commit pulls the pull of each commit is theta itself, so the
+ * next launch reads theta from that snapshot row and only a run's last
+ * launch writes the theta array. */
 int gem_stats(gem_t* g, gem_stats_t* out);
 int gem_stats_reset(gem_t* g);
 
@@ -368,8 +372,10 @@ int gem_load(gem_t* g, const char* path);
  * 256 MiB Infinity Cache stays there between passes (streaming it is 14-24%
  * slower).  GEM_CACHE_AUTO (the default) streams when theta, h, theta* and
  * the snapshot and moment table together exceed 256 MiB.  Results are the
- * same bits under every policy; the per-segment scope and the diagnostic
- * passes keep the default policy.  GEM_EINVAL for another value. */
+ * same bits under every policy.  The diagnostic passes keep the default
+ * policy; so do the per-segment scope's loads of h and theta*, which every
+ * commit reads: with the other streams non-temporal the Infinity Cache keeps
+ * them between commits.  GEM_EINVAL for another value. */
 int gem_set_cache_policy(gem_t* g, int32_t policy);
 
 /* Wait for all queued work of the handle. */

@@ -55,7 +55,7 @@ struct gem_handle {
     int64_t* seg_off = nullptr;      // [nseg + 1]
     int64_t* part_off = nullptr;     // [nseg + 1]
     int32_t* gseg = nullptr;         // [groups]
-    double* part = nullptr;          // [3][npart] group sums of the current commit
+    double* part = nullptr;          // [3][npart][4] wave sums of the current commit
     int32_t* pair_seg = nullptr;     // [nsup] (segment, index block) pairs
     int32_t* pair_blk = nullptr;
     int64_t* sup_off = nullptr;      // [nseg + 1] first index-block slot of each segment
@@ -343,7 +343,8 @@ int build_segments(gem_handle* g, const std::vector<int64_t>& off)
     bool ok = hipMalloc(&g->seg_off, off.size() * sizeof(int64_t)) == hipSuccess &&
               hipMalloc(&g->part_off, part_off.size() * sizeof(int64_t)) == hipSuccess &&
               hipMalloc(&g->gseg, gseg.size() * sizeof(int32_t)) == hipSuccess &&
-              hipMalloc(&g->part, static_cast<size_t>(3 * npart) * sizeof(double)) == hipSuccess &&
+              hipMalloc(&g->part, static_cast<size_t>(3 * npart * gemk::kWavesPerGroup) *
+                                      sizeof(double)) == hipSuccess &&
               hipMalloc(&g->pair_seg, pair_seg.size() * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&g->pair_blk, pair_blk.size() * sizeof(int32_t)) == hipSuccess &&
               hipMalloc(&g->sup_off, sup_off.size() * sizeof(int64_t)) == hipSuccess &&
@@ -429,12 +430,16 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
     f.hist_per_seg = g->hist_seg ? 1 : 0;
     f.hist = nullptr;
     f.diag = a.diag;
-    // Bytes per element-commit the launches move: theta read and written, the
-    // committing worker's snapshot read and its pull written, the moment read
-    // and written; generated updates read h and theta* and the pending
+    // Bytes per element-commit the launches move: theta read (and, with
+    // pre-commit pulls, written: otherwise the pull of each commit holds it
+    // for the next launch, and only a run's last launch writes the array),
+    // the committing worker's snapshot read and its pull written, the moment
+    // read and written; generated updates read h and theta* and the pending
     // commit's snapshot (to generate its update again), given updates read
     // the caller's update twice.
-    const double per_elem = src == Source::Generated ? 36.0 : src == Source::GivenF32 ? 32.0 : 28.0;
+    const bool post = g->hp.pull_mode == GEM_PULL_POST_COMMIT;
+    const double per_elem = (src == Source::Generated ? 36.0 : src == Source::GivenF32 ? 32.0 : 28.0) -
+                            (post ? 4.0 : 0.0);
     for (int64_t j = 0; j < T; ++j) {
         const int32_t w = worker[j];
         const int64_t t = g->t;
@@ -447,6 +452,10 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
         a.t = static_cast<uint32_t>(t);
         a.upd_prev = (upd && j > 0) ? upd[j - 1] : nullptr;
         a.upd_cur = upd ? upd[j] : nullptr;
+        // theta before the pending commit j - 1: the array at the start of
+        // the run, else the pull of commit j - 2 (post-commit pulls)
+        a.theta_row = (post && j >= 2) ? worker[j - 2] : -1;
+        a.store_theta = post ? 0 : 1;
         GEM_HIP(gemk::launch_seg_step(a, src, bf16_out, stream_rows(g), g->stream));
         // Histogram recording: this commit's rows, while there is room.
         f.hist = nullptr;
@@ -466,6 +475,8 @@ int run_segments(gem_handle* g, const int32_t* worker, int64_t T, Source src,
     a.apply = 1;
     a.start = 0;
     a.t = static_cast<uint32_t>(g->t);
+    a.theta_row = (post && T >= 2) ? worker[T - 2] : -1;
+    a.store_theta = 1;
     a.w_prev = worker[T - 1];
     a.m_row_prev = a.m_row;
     a.upd_prev = upd ? upd[T - 1] : nullptr;

@@ -74,6 +74,9 @@ enum class Source { Generated = 0, GivenF32 = 1, GivenBF16 = 2 };
 // levels, 256 groups per index block.
 constexpr int64_t kSegGroup = 1024;
 constexpr int64_t kSegBlock = 1 << 18;
+// The step kernel writes one partial sum per wave (256 indices); a group's
+// four follow each other in the partial-sum array.
+constexpr int64_t kWavesPerGroup = 4;
 
 // One launch of the segment step kernel: finish the pending commit (apply its
 // per-segment factors and pull) and/or start commit t (form d, m and the
@@ -88,7 +91,7 @@ struct SegArgs {
     const void* upd_prev;     // caller update of the pending commit (given updates)
     const void* upd_cur;      // caller update of commit t (given updates)
     const float* pi_seg;      // [nseg] factors of the pending commit
-    double* part;             // [3][npart] group sums of squares of commit t: drift, m, d
+    double* part;             // [3][npart][4] wave sums of squares of commit t: drift, m, d
     const int64_t* seg_off;   // [nseg + 1]
     const int64_t* part_off;  // [nseg + 1] first group-sum slot of each segment
     const int32_t* gseg;      // [groups] segment holding each group's first element
@@ -102,6 +105,12 @@ struct SegArgs {
     int32_t m_row;            // worker whose moment commit t refreshes
     int32_t m_row_prev;       // worker whose moment the pending commit refreshed (diagnostics)
     int32_t pre_pull;         // the snapshot keeps the pre-commit theta
+    // Where theta before the pending commit is read from: -1 for the theta
+    // array, else this worker's snapshot row (with post-commit pulls the
+    // previous commit's worker pulled exactly that theta, so the array need
+    // not be written between the launches of a run).
+    int32_t theta_row;
+    int32_t store_theta;      // write theta to the theta array (a run's last launch)
     double* diag;             // [4] accumulators, or null (diagnostic variant)
     float k_eff;              // kappa as it multiplies the moment (diagnostics)
     uint32_t t;               // clock of commit t; the pending commit's is t - 1

@@ -680,11 +680,10 @@ __device__ __forceinline__ void block_tree_sum3(double& x, double& y, double& z,
     __syncthreads();
 }
 
-// At least 7 waves per SIMD (72 VGPRs): the blocks' barrier phases leave the
-// memory pipes to the other waves; measured 3% faster than the 6 waves its
-// 74 VGPRs gave, while 8 waves spill and run 15% slower.
+// No occupancy hint: with no barrier in the kernel, the compiler's own
+// register budget runs 2.5% faster than a 7-waves-per-SIMD cap.
 template <Source SRC, bool BF16, bool DIAG, bool NT>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7, 8)))
+__global__ __launch_bounds__(kBlock)
 void seg_step_kernel(const SegArgs a)
 {
     static_assert(kBlock * 4 == kSegGroup, "one block per group of sums");
@@ -693,32 +692,56 @@ void seg_step_kernel(const SegArgs a)
     const int64_t c = grp * kBlock + threadIdx.x;
     const bool active = c < (a.Pp >> 2);   // the last group may hold fewer chunks
     const int64_t off = c * 4;
+    // The block's segments: its first, and whether the whole block lies in it
+    // (all but the blocks that hold a segment boundary), in which case every
+    // element takes that segment's factor and the block forms one set of
+    // sums.  The lookups are issued before the streaming loads, so their
+    // latency hides behind those instead of delaying the update.
     const int32_t s_first = a.gseg[grp];
+    const int64_t g_lo = grp * kSegGroup;
+    const int64_t g_hi = (g_lo + kSegGroup < a.P) ? g_lo + kSegGroup : a.P;
+    const int64_t s_lo = a.seg_off[s_first], s_hi = a.seg_off[s_first + 1];
+    const bool one_seg = s_hi >= g_hi;
+    const float pi_one = a.apply ? a.pi_seg[s_first] : 0.0f;
 
-    float4 th = active ? load4<NT>(a.theta + off) : make_float4(0.f, 0.f, 0.f, 0.f);
+    const float* th_src = a.theta_row < 0 ? a.theta + off
+                                          : a.S + tile_index(a.nw, a.theta_row, off);
+    float4 th = active ? load4<NT>(th_src) : make_float4(0.f, 0.f, 0.f, 0.f);
     const float4 th_old = th;
     float4 hv = make_float4(0.f, 0.f, 0.f, 0.f), tv = hv;
+    // h and theta* keep the default cache policy even when everything else
+    // streams: every commit reads them, and with the other streams marked
+    // non-temporal the Infinity Cache holds them from one launch to the next
+    // (measured 10% faster at 25M parameters).
     if (SRC == Source::Generated && active) {
-        hv = load4<NT>(a.h + off);
-        tv = load4<NT>(a.ts + off);
+        hv = load4<false>(a.h + off);
+        tv = load4<false>(a.ts + off);
     }
     // The rows this commit starts from, loaded with the others so that the
     // thread waits for memory once: the committing worker's snapshot (unused
     // when it is the pending worker, whose pull is stored below) and its
     // moment (no earlier store of this launch touches it).
+    // A row that holds theta_t is not read again: the committing worker's
+    // snapshot when it is the pending worker (it pulls below) or the worker
+    // whose row held theta_t.
+    const bool cur_pulls_now = a.apply && a.w_cur == a.w_prev;
     float4 s_cur = make_float4(0.f, 0.f, 0.f, 0.f), m_cur = s_cur;
     if (a.start && active) {
-        s_cur = load4<NT>(a.S + tile_index(a.nw, a.w_cur, off));
+        if (!cur_pulls_now && a.w_cur != a.theta_row)
+            s_cur = load4<NT>(a.S + tile_index(a.nw, a.w_cur, off));
         m_cur = load4<NT>(a.M + tile_index(a.nw, a.m_row, off));
     }
+    // The pending worker's snapshot, to generate its update again (and for
+    // the diagnostics' kinetic energy).
+    float* srow = a.S + tile_index(a.nw, a.w_prev, off);
+    float4 sp = make_float4(0.f, 0.f, 0.f, 0.f);
+    if ((SRC == Source::Generated || DIAG) && a.apply && active)
+        sp = a.w_prev == a.theta_row ? th_old : load4<NT>(srow);
     double ek = 0.0, proxy = 0.0;   // diagnostic variant: energies of the pending commit
     if (a.apply && active) {
         // The pending commit's update: the caller's, or generated again at
         // the worker's snapshot, which its pull below replaces.
         float4 d;
-        float* srow = a.S + tile_index(a.nw, a.w_prev, off);
-        float4 sp = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (SRC == Source::Generated || DIAG) sp = load4<NT>(srow);
         if (SRC == Source::Generated) {
             const float4 z = normals4(static_cast<uint64_t>(c), a.t - 1u, a.key0, a.key1);
             d.x = stale_update<BF16>(a.neg_lr, a.sigma, sp.x, hv.x, tv.x, z.x);
@@ -729,15 +752,22 @@ void seg_step_kernel(const SegArgs a)
             d = load_given<SRC>(a.upd_prev, c, a.P);
         }
         // eq. 3 with the factor of each element's segment (padding stays put)
-        int32_t seg = s_first;
-        auto factor = [&](int64_t i) {
-            while (a.seg_off[seg + 1] <= i) ++seg;
-            return a.pi_seg[seg];
-        };
-        if (off + 0 < a.P) th.x = __builtin_fmaf(factor(off + 0), d.x, th.x);
-        if (off + 1 < a.P) th.y = __builtin_fmaf(factor(off + 1), d.y, th.y);
-        if (off + 2 < a.P) th.z = __builtin_fmaf(factor(off + 2), d.z, th.z);
-        if (off + 3 < a.P) th.w = __builtin_fmaf(factor(off + 3), d.w, th.w);
+        if (one_seg) {
+            if (off + 0 < a.P) th.x = __builtin_fmaf(pi_one, d.x, th.x);
+            if (off + 1 < a.P) th.y = __builtin_fmaf(pi_one, d.y, th.y);
+            if (off + 2 < a.P) th.z = __builtin_fmaf(pi_one, d.z, th.z);
+            if (off + 3 < a.P) th.w = __builtin_fmaf(pi_one, d.w, th.w);
+        } else {
+            int32_t seg = s_first;
+            auto factor = [&](int64_t i) {
+                while (a.seg_off[seg + 1] <= i) ++seg;
+                return a.pi_seg[seg];
+            };
+            if (off + 0 < a.P) th.x = __builtin_fmaf(factor(off + 0), d.x, th.x);
+            if (off + 1 < a.P) th.y = __builtin_fmaf(factor(off + 1), d.y, th.y);
+            if (off + 2 < a.P) th.z = __builtin_fmaf(factor(off + 2), d.z, th.z);
+            if (off + 3 < a.P) th.w = __builtin_fmaf(factor(off + 3), d.w, th.w);
+        }
         store4<NT>(srow, pick(a.pre_pull, th_old, th));
         if (DIAG) {
             // E_k against the worker's snapshot (eq. 11) and the proxy energy
@@ -763,7 +793,7 @@ void seg_step_kernel(const SegArgs a)
         }
     }
     if (!a.start) {
-        if (active) store4<NT>(a.theta + off, th);
+        if (active && a.store_theta) store4<NT>(a.theta + off, th);
         return;
     }
 
@@ -772,7 +802,8 @@ void seg_step_kernel(const SegArgs a)
     s = mo;
     d = mo;
     if (active) {
-        if (a.apply && a.w_cur == a.w_prev) s = pick(a.pre_pull, th_old, th);   // just pulled
+        if (cur_pulls_now) s = pick(a.pre_pull, th_old, th);   // just pulled
+        else if (a.w_cur == a.theta_row) s = th_old;
         else s = s_cur;
         if (SRC == Source::Generated) {
             const float4 z = normals4(static_cast<uint64_t>(c), a.t, a.key0, a.key1);
@@ -791,7 +822,7 @@ void seg_step_kernel(const SegArgs a)
         m.z = __builtin_fmaf(a.mu, mo.z, d.z);
         m.w = __builtin_fmaf(a.mu, mo.w, d.w);
         store4<NT>(mrow, m);
-        store4<NT>(a.theta + off, th);
+        if (a.store_theta) store4<NT>(a.theta + off, th);
         mo = m;
     }
     // Terms of the sums of squares: drift theta_t - s_t (eq. 16), m and d.
@@ -807,12 +838,16 @@ void seg_step_kernel(const SegArgs a)
     }
     // One set of group sums per segment the group touches (terms outside the
     // segment count as zero); the loop is uniform across the block.
-    const int64_t g_lo = grp * kSegGroup;
-    const int64_t g_hi = (g_lo + kSegGroup < a.P) ? g_lo + kSegGroup : a.P;
-    for (int32_t seg = s_first; a.seg_off[seg] < g_hi; ++seg) {
-        const int64_t lo = a.seg_off[seg], hi = a.seg_off[seg + 1];
+    for (int32_t seg = s_first; seg == s_first || a.seg_off[seg] < g_hi; ++seg) {
+        const int64_t lo = seg == s_first ? s_lo : a.seg_off[seg];
+        const int64_t hi = seg == s_first ? s_hi : a.seg_off[seg + 1];
         double ca = 0.0, cm = 0.0, cd = 0.0;
-        if (active) {
+        if (one_seg && g_lo + kSegGroup <= a.P) {
+            // the whole group inside one segment and below P: no masks
+            ca = (ta[0] + ta[1]) + (ta[2] + ta[3]);
+            cm = (tm[0] + tm[1]) + (tm[2] + tm[3]);
+            cd = (td[0] + td[1]) + (td[2] + td[3]);
+        } else if (active) {
             double xa[4], xm[4], xd[4];
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -825,53 +860,67 @@ void seg_step_kernel(const SegArgs a)
             cm = (xm[0] + xm[1]) + (xm[2] + xm[3]);
             cd = (xd[0] + xd[1]) + (xd[2] + xd[3]);
         }
-        double sa = ca, sm = cm, sd = cd;
-        block_tree_sum3(sa, sm, sd, lds);
-        if (threadIdx.x == 0) {
-            const int64_t q = a.part_off[seg] + (grp - (lo / kSegGroup));
-            a.part[q] = sa;
-            a.part[a.npart + q] = sm;
-            a.part[2 * a.npart + q] = sd;
+        // The wave's 256-index subtree (lane butterflies add pairs 2k, 2k+1,
+        // then pairs of pairs, ...); seg_blocks_kernel adds the group's four
+        // wave sums as (w0 + w1) + (w2 + w3), the next level of the same
+        // tree.  No barrier: each wave writes its own slot.
+#pragma unroll
+        for (int mask = 1; mask < 64; mask <<= 1) {
+            ca = ca + __shfl_xor(ca, mask);
+            cm = cm + __shfl_xor(cm, mask);
+            cd = cd + __shfl_xor(cd, mask);
         }
+        if ((threadIdx.x & 63) == 0) {
+            const int64_t q = (a.part_off[seg] + (grp - (lo / kSegGroup))) * kWavesPerGroup +
+                              (threadIdx.x >> 6);
+            const int64_t stride = a.npart * kWavesPerGroup;
+            a.part[q] = ca;
+            a.part[stride + q] = cm;
+            a.part[2 * stride + q] = cd;
+        }
+        if (one_seg) break;
     }
 }
 
-// Lane k's binary64 value, read by every lane (the two halves through the
-// scalar unit).
-__device__ __forceinline__ double read_lane(double v, int k)
+// The lanes of one wave see each other's LDS writes made before this point.
+__device__ __forceinline__ void wave_sync()
 {
-    const uint64_t b = static_cast<uint64_t>(__double_as_longlong(v));
-    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(b)), k);
-    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(b >> 32)), k);
-    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // One wave (threadIdx.x < 64): add segment seg's index-block sums in
-// increasing order (the lanes load 64 at a time; the additions stay in
-// order, on values read lane by lane), take the norms (binary64 square root,
+// increasing order (the lanes load 64 at a time into LDS; lane 0 adds them
+// in order), take the norms (binary64 square root,
 // rounded to binary32) and form pi as in the element step (eq. 18 with norms).
 __device__ void reduce_segment(int32_t seg, const double* sup, int64_t nsup,
                                const int64_t* __restrict__ sup_off, float* __restrict__ pi_seg,
                                float k_eff, float eps, int32_t literal,
                                const int64_t* __restrict__ seg_off, uint32_t* hist,
-                               int32_t hist_per_seg, double* diag)
+                               int32_t hist_per_seg, double* diag, double (*tail)[64])
 {
     const int64_t q0 = sup_off[seg], q1 = sup_off[seg + 1];
     double sa = 0.0, sm = 0.0, sd = 0.0;
     for (int64_t base = q0; base < q1; base += 64) {
+        // the lanes load 64 block sums of each kind at once into LDS; lane 0
+        // then adds them in order (one wave: its LDS accesses stay in order)
         const int64_t q = base + threadIdx.x;
-        double va = 0.0, vm = 0.0, vd = 0.0;
         if (q < q1) {
-            va = sup[q];
-            vm = sup[nsup + q];
-            vd = sup[2 * nsup + q];
+            tail[0][threadIdx.x] = sup[q];
+            tail[1][threadIdx.x] = sup[nsup + q];
+            tail[2][threadIdx.x] = sup[2 * nsup + q];
         }
-        const int cnt = (q1 - base < 64) ? static_cast<int>(q1 - base) : 64;
-        for (int k = 0; k < cnt; ++k) {
-            sa = sa + read_lane(va, k);
-            sm = sm + read_lane(vm, k);
-            sd = sd + read_lane(vd, k);
+        wave_sync();
+        if (threadIdx.x == 0) {
+            const int cnt = (q1 - base < 64) ? static_cast<int>(q1 - base) : 64;
+            for (int k = 0; k < cnt; ++k) {
+                sa = sa + tail[0][k];
+                sm = sm + tail[1][k];
+                sd = sd + tail[2][k];
+            }
         }
+        wave_sync();
     }
     if (threadIdx.x != 0) return;
     const float na = static_cast<float>(sqrt(sa));
@@ -915,6 +964,7 @@ __global__ __launch_bounds__(kBlock) void seg_blocks_kernel(const double* __rest
 {
     static_assert(kBlock * kSegGroup == kSegBlock, "one thread per group of an index block");
     __shared__ double lds[3][4];
+    __shared__ double tail[3][64];
     __shared__ int last;
     const int32_t seg = pair_seg[blockIdx.x];
     const int64_t blk = pair_blk[blockIdx.x];
@@ -923,10 +973,16 @@ __global__ __launch_bounds__(kBlock) void seg_blocks_kernel(const double* __rest
     const int64_t grp = blk * kBlock + threadIdx.x;
     double va = 0.0, vm = 0.0, vd = 0.0;
     if (grp >= g_lo && grp <= g_hi) {
-        const int64_t q = part_off[seg] + (grp - g_lo);
-        va = part[q];
-        vm = part[npart + q];
-        vd = part[2 * npart + q];
+        // the group's four wave sums, (w0 + w1) + (w2 + w3)
+        static_assert(kWavesPerGroup == 4, "four waves per group");
+        const int64_t q = (part_off[seg] + (grp - g_lo)) * kWavesPerGroup;
+        const int64_t stride = npart * kWavesPerGroup;
+        const double* pa = part + q;
+        const double* pm = part + stride + q;
+        const double* pd = part + 2 * stride + q;
+        va = (pa[0] + pa[1]) + (pa[2] + pa[3]);
+        vm = (pm[0] + pm[1]) + (pm[2] + pm[3]);
+        vd = (pd[0] + pd[1]) + (pd[2] + pd[3]);
     }
     double sa = va, sm = vm, sd = vd;
     block_tree_sum3(sa, sm, sd, lds);
@@ -946,7 +1002,7 @@ __global__ __launch_bounds__(kBlock) void seg_blocks_kernel(const double* __rest
     __threadfence();       // acquire the other blocks' sums
     if (threadIdx.x < 64)
         reduce_segment(seg, sup, nsup, sup_off, f.pi_seg, f.k_eff, f.eps, f.literal, seg_off,
-                       f.hist, f.hist_per_seg, f.diag);
+                       f.hist, f.hist_per_seg, f.diag, tail);
 }
 
 template <bool BF16>
