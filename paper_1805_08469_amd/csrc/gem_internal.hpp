@@ -55,7 +55,11 @@ struct PassArgs {
     int32_t K;
     float neg_lr, sigma, mu, eps, k_eff;
     uint32_t mode;
-    int32_t pad_;
+    // Streaming passes (NT) still read theta (keep_theta) or h and theta*
+    // (keep_problem) with the default policy when those vectors fit the
+    // Infinity Cache beside the streamed rows, which then serves them from
+    // one pass to the next.
+    uint8_t keep_theta, keep_problem, pad_[2];
     int32_t worker[GEM_K_MAX];
     int32_t tau[GEM_K_MAX];  // staleness (adaptive-staleness rule only)
     // 32-bit so that a uniform per-commit read is a scalar load: gfx9 has no

@@ -531,10 +531,16 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     Rows ring[DEPTH];
     Held held{};
     if (ch.active) {
-        ch.th = load4_at<NT>(a.theta + ch.blk0, ch.t16);
+        ch.th = a.keep_theta ? load4_at<false>(a.theta + ch.blk0, ch.t16)
+                             : load4_at<NT>(a.theta + ch.blk0, ch.t16);
         if (SRC == Source::Generated) {
-            ch.hh = load4_at<NT>(a.h + ch.blk0, ch.t16);
-            ch.tt = load4_at<NT>(a.ts + ch.blk0, ch.t16);
+            if (a.keep_problem) {
+                ch.hh = load4_at<false>(a.h + ch.blk0, ch.t16);
+                ch.tt = load4_at<false>(a.ts + ch.blk0, ch.t16);
+            } else {
+                ch.hh = load4_at<NT>(a.h + ch.blk0, ch.t16);
+                ch.tt = load4_at<NT>(a.ts + ch.blk0, ch.t16);
+            }
         }
 #pragma unroll
         for (int u = 0; u < DEPTH; ++u) {
@@ -596,7 +602,10 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
             held = so.held;
         }
     }
-    if (ch.active) store4_at<NT>(a.theta + ch.blk0, ch.t16, ch.th);
+    if (ch.active) {
+        if (a.keep_theta) store4_at<false>(a.theta + ch.blk0, ch.t16, ch.th);
+        else store4_at<NT>(a.theta + ch.blk0, ch.t16, ch.th);
+    }
     if (global_m && ch.active) store4_at<NT>(a.M + ch.tile, ch.io, ch.mg);
 
     if (DIAG && a.diag) {
