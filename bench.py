@@ -408,7 +408,11 @@ def main() -> int:
             "avg_launch_ms": avg_pass_s * 1e3,
             "kernel": (("seg_step_kernel + seg_blocks_kernel" + (", streaming" if streaming else ""))
                        if args.pi_scope == "segment"
-                       # recording takes the diagnostic variant: ring depth 2, default policy
+                       # the default rule records through its recording pass; the
+                       # other variants through the diagnostic one (depth 2, default policy)
+                       else "pass_kernel<Generated, Fast, recording, depth %d%s>"
+                       % (depth, ", streaming" if streaming else "")
+                       if args.pi_hist and variant == "Fast"
                        else "pass_kernel<Generated, %s, diagnostic, depth 2>" % variant
                        if args.pi_hist
                        else "pass_kernel<Generated, %s, depth %d%s>"

@@ -63,6 +63,7 @@ struct gem_handle {
     float* pi_seg = nullptr;         // [nseg]
     uint32_t* seg_done = nullptr;    // [nseg] pair blocks finished in the running launch
     uint32_t deep_lds = 0;           // LDS reserved per block of the deep-ring pass
+    int32_t cus = 0;                 // compute units of the device (0 if unknown)
     int64_t npart = 0;
     int64_t nsup = 0;
     void* scratch = nullptr;         // this device's static scratch (gem_gather_static)
@@ -228,7 +229,7 @@ void base_args(const gem_handle* g, PassArgs& a)
 int pass_depth(const gem_handle* g, Source src, int64_t kmax)
 {
     const bool deep = src == Source::Generated && kernel_variant(g->hp) == gemk::Variant::Fast &&
-                      kmax >= gemk::kDeepMinK && !g->diag_on && !g->hist_on;
+                      kmax >= gemk::kDeepMinK && !g->diag_on && (!g->hist_on || g->hist_rows == 1);
     return deep ? gemk::kPrefetchDeep : gemk::kPrefetchShallow;
 }
 
@@ -287,8 +288,15 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
         a.diag = g->diag_on ? g->acc : nullptr;
         a.hist_first = g->hist_count;
         a.hist_cap = g->hist_cap;
-        GEM_HIP(gemk::launch_pass(a, src, variant, bf16_out, g->diag_on || hist, depth, stream,
-                                  g->deep_lds, g->stream));
+        // Recording one histogram per commit on the fast path: the recording
+        // variant of the same pass; otherwise recording takes the diagnostic
+        // variant.
+        const bool rec = hist && !g->diag_on && g->hist_rows == 1 && src == Source::Generated &&
+                         variant == gemk::Variant::Fast;
+        // a recording pass loops 8 blocks per compute unit over the groups
+        a.rec_grid = rec ? 8 * g->cus : 0;
+        GEM_HIP(gemk::launch_pass(a, src, variant, bf16_out, (g->diag_on || hist) && !rec, rec,
+                                  depth, stream, g->deep_lds, g->stream));
         if (g->hist_on) g->hist_count += p.K;
         for (int j = 0; j < p.K; ++j) g->pc[p.worker[j]] = next_pull(g, g->t + j);
         g->t += p.K;
@@ -597,6 +605,11 @@ int gem_create(int64_t P, int32_t n, const gem_hyperparams* hp, void* stream, ge
             g->deep_lds = gemk::deep_lds_bytes(lds);
         else
             (void)hipGetLastError();   // no cap: the pass runs as its registers allow
+        if (hipDeviceGetAttribute(&g->cus, hipDeviceAttributeMultiprocessorCount, g->device) !=
+            hipSuccess) {
+            (void)hipGetLastError();
+            g->cus = 0;
+        }
     }
     // NULL is the device's null stream, which is also torch's default stream.
     g->stream = static_cast<hipStream_t>(stream);

@@ -43,7 +43,7 @@ struct PassArgs {
     const int64_t* hseg_off; // [hist_rows + 1] segment offsets (per-segment mode)
     const int32_t* hseg_grp; // [groups] segment of each 1024-element group's first element
     int32_t hist_rows;
-    int32_t hist_pad_;
+    int32_t rec_grid;        // blocks of a recording pass (0: one per group of 1024 elements)
     float* sink_S;           // [kSinkChunks * 4] target of loads/stores a step does not need
     float* sink_M;
     int64_t sink_mask;       // kSinkChunks - 1
@@ -133,8 +133,11 @@ enum class Variant { General = 0, Fast = 1, FastGlobal = 2 };
 // stream_rows: non-temporal row and vector accesses (the diagnostic variant
 // ignores it).  deep_lds: dynamic LDS bytes reserved per block of the
 // deep-ring pass (deep_lds_bytes), 0 for none.
+// rec: the fast recording pass (Generated, Fast, no diagnostics; one
+// histogram per commit in a.pi_hist).
 hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
-                       int depth, bool stream_rows, uint32_t deep_lds, hipStream_t stream);
+                       bool rec, int depth, bool stream_rows, uint32_t deep_lds,
+                       hipStream_t stream);
 
 
 // Infinity Cache of one MI355X: a state this small stays cached across passes.

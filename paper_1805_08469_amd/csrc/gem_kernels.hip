@@ -60,6 +60,12 @@ constexpr int kBlock = 256;
 // elements of further segments count straight into memory.
 constexpr int kHistLdsSegs = 8;
 
+// Recording pass (REC): the block keeps one histogram per commit of the pass
+// in LDS for the whole pass, two bins per 32-bit word (16-bit counts: a block
+// counts at most 1024 elements per commit), cleared once before the pass and
+// flushed once after it -- no barrier between commits.
+constexpr int kRecWords = (GEM_PI_BINS + 1) / 2;
+
 struct DiagAcc {
     double ek = 0.0, proxy = 0.0, clamped = 0.0, elems = 0.0;
     uint32_t* hist = nullptr;   // block-local histograms of the current commit (LDS)
@@ -94,7 +100,8 @@ __device__ __forceinline__ int scale_bin(float x)
 // operand, which may then reach div_rn_core: its quotient is NaN there as in
 // the general division, and the clamp makes either pi = 0.
 __device__ __forceinline__ void commit4_fast(const PassArgs& a, const float4& d, const float4& s,
-                                             float4& th, float4& m, float4& snap)
+                                             float4& th, float4& m, float4& snap,
+                                             float* pi_out = nullptr)
 {
     const float dv[4] = {d.x, d.y, d.z, d.w};
     const float sv[4] = {s.x, s.y, s.z, s.w};
@@ -130,6 +137,7 @@ __device__ __forceinline__ void commit4_fast(const PassArgs& a, const float4& d,
     for (int k = 0; k < 4; ++k) {
         const float pi = (q[k] > 0.0f) ? q[k] : 0.0f;               // eq. 18, clamped
         tv[k] = __builtin_fmaf(pi, dv[k], tv[k]);                   // eq. 3
+        if (pi_out) pi_out[k] = pi;
     }
     th = make_float4(tv[0], tv[1], tv[2], tv[3]);
     snap = th;
@@ -390,9 +398,9 @@ struct StepOut {
 // row-pair load unconditionally -- those a step does not need go to the small
 // sink buffer, which stays in cache -- so the wait for a step's rows never
 // covers the loads issued after them.
-template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH, bool NT>
+template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH, bool NT, bool REC>
 __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch, Rows ring,
-                                             Held held, DiagAcc& acc)
+                                             Held held, DiagAcc& acc, uint32_t* rec_lds)
 {
     const uint32_t route = a.routes[j];
     const uint32_t src = route & kRouteSlotMask;
@@ -444,7 +452,36 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     StepOut r;
     r.out.m = rows.m;
     if constexpr (FAST && !DIAG) {
-        commit4_fast(a, d, rows.s, ch.th, r.out.m, r.out.s);
+        float pis[4];
+        commit4_fast(a, d, rows.s, ch.th, r.out.m, r.out.s, REC ? pis : nullptr);
+        if constexpr (REC) {
+            // this commit's factors into the block's LDS histogram (uniform
+            // test: recording stops at the capacity)
+            if (ch.active && a.hist_first + j < a.hist_cap) {
+                uint32_t* row = rec_lds + j * kRecWords;
+                uint32_t* spare = rec_lds + a.K * kRecWords + threadIdx.x;   // this lane's own word
+                const bool live[4] = {ch.l0, ch.l1, ch.l2, ch.l3};
+                // Clamped factors (+0, bin 0) are often most of a commit's:
+                // the wave counts them with ballots and adds them once, while
+                // their lanes (and padding elements) add to a word of their
+                // own, so no add waits behind one address and no lane
+                // branches.  A positive factor's bin is scale_bin's, in
+                // integer steps: (bits >> 19) - 1710 clamped to [1, 642].
+                uint32_t clamped = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t bits = __float_as_uint(pis[k]);   // +0 or positive
+                    const bool counted = live[k] && bits != 0u;
+                    clamped += static_cast<uint32_t>(__popcll(__ballot(live[k] && bits == 0u)));
+                    const int bin = min(max(static_cast<int>(bits >> 19) - 1710, 1), GEM_PI_BINS - 1);
+                    uint32_t* word = counted ? row + (bin >> 1) : spare;
+                    atomicAdd(word, 1u << ((bin & 1) << 4));
+                }
+                const uint64_t lanes = __ballot(1);
+                if (clamped != 0u && (threadIdx.x & 63u) == static_cast<uint32_t>(__builtin_ctzll(lanes)))
+                    atomicAdd(&row[0], clamped);   // bin 0: the low half of word 0
+            }
+        }
     } else {
         commit_element<FAST, DIAG>(a, tau, d.x, rows.s.x, ch.th.x, r.out.m.x, r.out.s.x, ch.active && ch.l0, acc, hrow[0]);
         commit_element<FAST, DIAG>(a, tau, d.y, rows.s.y, ch.th.y, r.out.m.y, r.out.s.y, ch.active && ch.l1, acc, hrow[1]);
@@ -490,18 +527,20 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     return r;
 }
 
-template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH, bool NT>
-__global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
+// One pass over the 1024 elements of group grp (the block's 256 chunks).
+template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH, bool NT, bool REC>
+__device__ __forceinline__ void pass_group(const PassArgs& a, int64_t grp, uint32_t* rec_lds)
 {
+    static_assert(!(REC && DIAG), "recording passes take the fast commit");
     const int64_t nchunk = a.Pp >> 2;
-    const int64_t c = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const int64_t c = grp * kBlock + threadIdx.x;
     Chunk ch;
     ch.active = c < nchunk;
-    if (!DIAG && !ch.active) return;
+    if (!DIAG && !ch.active) return;   // (the diagnostic variant's barriers need every thread)
     ch.c = ch.active ? c : 0;   // inactive lanes (diagnostic variant) do no memory work
     ch.off = ch.c * 4;
     static_assert((kBlock & (kBlock - 1)) == 0, "block size a power of two");
-    ch.q_hi = static_cast<uint32_t>((static_cast<int64_t>(blockIdx.x) * kBlock) >> 32);
+    ch.q_hi = static_cast<uint32_t>((grp * kBlock) >> 32);
     ch.q_lo = static_cast<uint32_t>(ch.c);
     ch.l0 = ch.off + 0 < a.P;
     ch.l1 = ch.off + 1 < a.P;
@@ -515,7 +554,7 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
                           (V == Variant::General && (a.mode & kModeGlobalProxy));
     static_assert(kTileElems % (kBlock * 4) == 0, "a block's chunks lie in one tile");
     static_assert(kSinkChunks % kBlock == 0, "a block's sink entries are contiguous");
-    ch.blk0 = static_cast<int64_t>(blockIdx.x) * (kBlock * 4);
+    ch.blk0 = grp * (kBlock * 4);
     ch.t16 = threadIdx.x * 16u;
     ch.tile = tile_index(a.nw, 0, ch.blk0 & ~(kTileElems - 1));
     ch.tin = ch.blk0 & (kTileElems - 1);
@@ -566,9 +605,9 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
             acc.hist = hist_lds;
             if (a.hist_rows > 1) {
                 // The block's segments (uniform) and each element's segment.
-                const int64_t g_lo = static_cast<int64_t>(blockIdx.x) * kBlock * 4;
+                const int64_t g_lo = grp * kBlock * 4;
                 const int64_t g_last = (g_lo + kBlock * 4 < a.P ? g_lo + kBlock * 4 : a.P) - 1;
-                acc.seg_first = a.hseg_grp[blockIdx.x];
+                acc.seg_first = a.hseg_grp[grp];
                 int32_t seg_last = acc.seg_first;
                 while (a.hseg_off[seg_last + 1] <= g_last) ++seg_last;
                 const int32_t rows = seg_last - acc.seg_first + 1;
@@ -588,7 +627,8 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
     for (; j + DEPTH <= K; j += DEPTH) {
 #pragma unroll
         for (int u = 0; u < DEPTH; ++u) {
-            const StepOut so = pass_step<SRC, V, BF16, DIAG, DEPTH, NT>(a, j + u, ch, ring[u], held, acc);
+            const StepOut so = pass_step<SRC, V, BF16, DIAG, DEPTH, NT, REC>(a, j + u, ch, ring[u], held,
+                                                                            acc, rec_lds);
             ring[u] = so.next;
             held = so.held;
         }
@@ -597,7 +637,8 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
 #pragma unroll
     for (int u = 0; u + 1 < DEPTH; ++u) {
         if (j + u < K) {
-            const StepOut so = pass_step<SRC, V, BF16, DIAG, DEPTH, NT>(a, j + u, ch, ring[u], held, acc);
+            const StepOut so = pass_step<SRC, V, BF16, DIAG, DEPTH, NT, REC>(a, j + u, ch, ring[u], held,
+                                                                            acc, rec_lds);
             ring[u] = so.next;
             held = so.held;
         }
@@ -623,6 +664,36 @@ __global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
             __syncthreads();
         }
         if (threadIdx.x < 4) atomicAdd(&a.diag[threadIdx.x], red[threadIdx.x][0]);
+    }
+}
+
+// The fused pass: one group per block; the recording variant (REC) loops its
+// blocks over the groups (a grid of a.rec_grid blocks, 0 for one per group)
+// so that each block's per-pass LDS histograms gather many groups before
+// their single flush -- one global atomic per nonzero bin and block.
+template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH, bool NT, bool REC>
+__global__ __launch_bounds__(kBlock) void pass_kernel(const PassArgs a)
+{
+    extern __shared__ uint32_t dyn_lds[];   // REC: K rows of kRecWords, then a word per thread
+    if constexpr (REC) {
+        for (int w = threadIdx.x; w < a.K * kRecWords; w += kBlock) dyn_lds[w] = 0u;
+        __syncthreads();
+        const int64_t ngroups = ((a.Pp >> 2) + kBlock - 1) / kBlock;
+        for (int64_t grp = blockIdx.x; grp < ngroups; grp += gridDim.x)
+            pass_group<SRC, V, BF16, DIAG, DEPTH, NT, REC>(a, grp, dyn_lds);
+        // the histograms into the recording, one atomic per nonzero bin
+        __syncthreads();
+        for (int w = threadIdx.x; w < a.K * kRecWords; w += kBlock) {
+            const uint32_t v = dyn_lds[w];
+            const int j = w / kRecWords;
+            if (v == 0u || a.hist_first + j >= a.hist_cap) continue;
+            uint32_t* row = a.pi_hist + (a.hist_first + j) * GEM_PI_BINS;
+            const int b = 2 * (w - j * kRecWords);
+            if (v & 0xFFFFu) atomicAdd(&row[b], v & 0xFFFFu);
+            if (v >> 16) atomicAdd(&row[b + 1], v >> 16);
+        }
+    } else {
+        pass_group<SRC, V, BF16, DIAG, DEPTH, NT, REC>(a, blockIdx.x, dyn_lds);
     }
 }
 
@@ -1141,12 +1212,35 @@ inline unsigned blocks_for(int64_t items) {
 
 // lds: bytes of dynamic LDS reserved per block (unused by the kernel), which
 // caps the blocks a CU holds at once.
-template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH, bool NT>
+template <Source SRC, Variant V, bool BF16, bool DIAG, int DEPTH, bool NT, bool REC = false>
 hipError_t launch_one(const PassArgs& a, hipStream_t st, uint32_t lds = 0)
 {
-    hipLaunchKernelGGL((pass_kernel<SRC, V, BF16, DIAG, DEPTH, NT>), dim3(blocks_for(a.Pp >> 2)),
-                       dim3(kBlock), lds, st, a);
+    if (REC) {
+        // K histograms, then one spare word per thread
+        const uint32_t need = (static_cast<uint32_t>(a.K) * kRecWords + kBlock) * 4u;
+        lds = lds > need ? lds : need;
+    }
+    unsigned grid = blocks_for(a.Pp >> 2);
+    if (REC && a.rec_grid > 0 && static_cast<unsigned>(a.rec_grid) < grid)
+        grid = static_cast<unsigned>(a.rec_grid);
+    hipLaunchKernelGGL((pass_kernel<SRC, V, BF16, DIAG, DEPTH, NT, REC>), dim3(grid), dim3(kBlock),
+                       lds, st, a);
     return hipGetLastError();
+}
+
+// Recording passes of the default rule with per-worker moments on generated
+// updates (one histogram per commit).
+template <bool BF16>
+hipError_t launch_rec(const PassArgs& a, int depth, bool stream, uint32_t deep_lds, hipStream_t st)
+{
+    constexpr Source G = Source::Generated;
+    constexpr Variant F = Variant::Fast;
+    if (depth == kPrefetchDeep)
+        return stream ? launch_one<G, F, BF16, false, kPrefetchDeep, true, true>(a, st, deep_lds)
+                      : launch_one<G, F, BF16, false, kPrefetchDeep, false, true>(a, st, deep_lds);
+    if (depth != kPrefetchShallow) return hipErrorInvalidValue;
+    return stream ? launch_one<G, F, BF16, false, kPrefetchShallow, true, true>(a, st)
+                  : launch_one<G, F, BF16, false, kPrefetchShallow, false, true>(a, st);
 }
 
 // The diagnostic variant keeps the default cache policy.
@@ -1184,8 +1278,14 @@ hipError_t launch_fd(const PassArgs& a, Variant v, bool diag, int depth, bool st
 }  // namespace
 
 hipError_t launch_pass(const PassArgs& a, Source src, Variant v, bool bf16_out, bool diag,
-                       int depth, bool stream_rows, uint32_t deep_lds, hipStream_t stream)
+                       bool rec, int depth, bool stream_rows, uint32_t deep_lds,
+                       hipStream_t stream)
 {
+    if (rec) {
+        if (src != Source::Generated || v != Variant::Fast || diag) return hipErrorInvalidValue;
+        return bf16_out ? launch_rec<true>(a, depth, stream_rows, deep_lds, stream)
+                        : launch_rec<false>(a, depth, stream_rows, deep_lds, stream);
+    }
     switch (src) {
     case Source::Generated:
         return bf16_out ? launch_fd<Source::Generated, true>(a, v, diag, depth, stream_rows,

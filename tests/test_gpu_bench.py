@@ -13,7 +13,8 @@ pytestmark = pytest.mark.gpu
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 CASES = [
-    (["--pi-hist"], "diagnostic, depth 2"),
+    (["--pi-hist"], "Fast, recording"),
+    (["--pi-hist", "--proxy", "global"], "FastGlobal, diagnostic, depth 2"),
     (["--cache", "stream"], "streaming"),
     (["--pi-scope", "segment"], "seg_step_kernel + seg_blocks_kernel"),
     (["--proxy", "global", "--cache", "keep"], "FastGlobal"),

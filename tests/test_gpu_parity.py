@@ -353,6 +353,34 @@ def test_pi_histograms_match_oracle(G, mode):
     assert_parity("theta", theta, st.theta)
 
 
+@pytest.mark.parametrize("K,bf16,cap", [(16, False, 120), (32, False, 150), (8, False, 77),
+                                        (32, True, 100)])
+def test_pi_histograms_recording_pass_match_oracle(G, K, bf16, cap):
+    """The default rule without energy diagnostics records through its own
+    pass (one LDS histogram per commit for the whole pass, flushed once):
+    counts exact against the oracle, in deep (K >= 16) and shallow passes, with
+    bf16 updates, a ragged tail and the capacity reached inside a pass."""
+    from paper_1805_08469_amd.workloads import make_problem
+    P, n, T = 6000 + 7, 5, 150
+    hp = _hp(G)
+    h, ts = make_problem(P, 1e-3, 1.0, 3)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=7)
+    with G.Gem(P, n, hp) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 2, bf16=bf16)
+        G.gem_pi_hist_start(g.h, cap)
+        g.sim_run(worker, tau, K)
+        got = G.gem_pi_hist_read(g.h, T)
+        theta, S, M = g.theta(), g.S(), g.M()
+    st = O.State.initial(n, P)
+    _, _, hist = O.run(_ohp(hp, 0.01, 0.1, 2, bf16=bf16), P, st, np.arange(P), h, ts, worker, tau, pi_hist=True)
+    assert got.shape == (min(cap, T), G.GEM_PI_BINS)
+    assert np.array_equal(got, hist[:cap])
+    assert got.sum(axis=1).tolist() == [P] * min(cap, T)
+    assert_parity("theta", theta, st.theta)
+    assert_parity("S", S, st.S)
+    assert_parity("M", M, st.M)
+
+
 # Partitions for per-segment histograms: one segment; tensors inside and across
 # the 1024-element blocks; a block holding more segments than it keeps
 # block-local histograms for (the rest count straight into memory).
