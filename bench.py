@@ -251,6 +251,9 @@ def main() -> int:
                          "outgrows the Infinity Cache), the default policy, or streaming")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle timing (profiling runs)")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the copy-ceiling and compute-floor measurements after the timed "
+                         "steps (profiling runs: they launch the same kernels on other shapes)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the copy kernel (counter calibration) and exit")
     ap.add_argument("--compare", action="store_true",
@@ -344,11 +347,11 @@ def main() -> int:
     stats = G.gem_stats(g.h)
     assert stats.commits == args.steps * wl.T
     g.close()
-    copy_gbs = copy_ceiling(G, torch, 2 << 30)
+    copy_gbs = None if args.no_ceilings else copy_ceiling(G, torch, 2 << 30)
     # The compute floor of a pass of K commits (not defined for the
     # per-segment scope, whose commits are not fused).
     floor_ms = (compute_floor(G, torch, wl, hp, cache, args.pi_hist) * wl.K
-                if args.pi_scope == "element" else None)
+                if args.pi_scope == "element" and not args.no_ceilings else None)
 
     elapsed = max(gpu_s, 1e-12)
     value = wl.P * stats.commits / elapsed
@@ -365,7 +368,7 @@ def main() -> int:
     # The pass is reported against the ceiling it is nearer to: the compute
     # floor of its arithmetic, or the library's copy rate on HBM.  A pass far
     # from both (a launch-bound one over a tiny vector) keeps the HBM roofline.
-    if floor_share is not None and floor_share > max(achieved / copy_gbs, 0.5):
+    if floor_share is not None and copy_gbs and floor_share > max(achieved / copy_gbs, 0.5):
         valu = cnt.get("valu_instrs_per_pass") if cnt else None
         ach = valu / avg_pass_s / 1e9 if valu else None
         roof = {"bound": "alu", "achieved": ach, "peak": VALU_PEAK_GINST,
@@ -418,7 +421,7 @@ def main() -> int:
                        else "pass_kernel<Generated, %s, depth %d%s>"
                        % (variant, depth, ", streaming" if streaming else "")),
             "copy_ceiling_GBps": copy_gbs,
-            "frac_of_copy": achieved / copy_gbs,
+            "frac_of_copy": achieved / copy_gbs if copy_gbs else None,
             "compute_floor_ms": floor_ms,
             "frac_of_compute_floor": floor_share,
         },

@@ -195,11 +195,20 @@ __device__ __forceinline__ void sincos_of_turn(uint32_t k, float& sn, float& cs)
     pc = __builtin_fmaf(pc, x2, -0.5f);
     const float cx = __builtin_fmaf(pc, x2, 1.0f);
 
-    const uint32_t q = quarter & 3u;
-    const float a = (q & 1u) ? cx : sx;     // |sin| candidate
-    const float b = (q & 1u) ? sx : cx;     // |cos| candidate
-    sn = (q >= 2u) ? -a : a;
-    cs = (q == 1u || q == 2u) ? -b : b;
+    // Quadrant q = quarter mod 4 (bits 22 and 23 of k + 2^21): sin takes sx, cx,
+    // -sx, -cx and cos cx, -sx, -cx, sx.  On the bits: an odd quadrant swaps
+    // the two (a bit-select under a mask of bit 22), quadrants 2 and 3 negate
+    // sin (bit 23 into the sign) and quadrants 1 and 2 negate cos (bit 22 xor
+    // bit 23) -- negation flips the sign bit, as -x does.
+    const uint32_t kq = k + 0x00200000u;
+    const uint32_t odd = static_cast<uint32_t>(static_cast<int32_t>(kq << 9) >> 31);
+    const uint32_t sxb = __float_as_uint(sx), cxb = __float_as_uint(cx);
+    const uint32_t a = (odd & cxb) | (~odd & sxb);     // |sin| candidate
+    const uint32_t b = (odd & sxb) | (~odd & cxb);     // |cos| candidate
+    const uint32_t neg_s = (kq << 8) & 0x80000000u;
+    const uint32_t neg_c = ((kq << 8) ^ (kq << 9)) & 0x80000000u;
+    sn = __uint_as_float(a ^ neg_s);
+    cs = __uint_as_float(b ^ neg_c);
 }
 
 // Box-Muller (1958): from two words, u1 = ((xa >> 8) + 1) 2^-24 in (0, 1] and

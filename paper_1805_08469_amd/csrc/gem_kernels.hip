@@ -125,19 +125,26 @@ __device__ __forceinline__ void commit4_fast(const PassArgs& a, const float4& d,
         hi = __builtin_fmaxf(hi, __builtin_fabsf(den[k]));
         lo = __builtin_fminf(lo, __builtin_fabsf(den[k]));
     }
-    float q[4];
+    // eq. 18, clamped at +0 (pi = q > 0 ? q : +0).  In the core range every
+    // quotient is finite, so the clamp is the signed-integer maximum of its
+    // bits with 0 (negative values and -0 have the sign bit set): one
+    // instruction, where the float form needs a canonicalisation as well.
+    float pi[4];
     if (lo >= 0x1p-60f && hi <= 0x1p60f) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) q[k] = div_rn_core(num[k], den[k]);
+        for (int k = 0; k < 4; ++k)
+            pi[k] = __int_as_float(max(__float_as_int(div_rn_core(num[k], den[k])), 0));
     } else {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) q[k] = div_rn(num[k], den[k]);
+        for (int k = 0; k < 4; ++k) {
+            const float q = div_rn(num[k], den[k]);
+            pi[k] = (q > 0.0f) ? q : 0.0f;
+        }
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-        const float pi = (q[k] > 0.0f) ? q[k] : 0.0f;               // eq. 18, clamped
-        tv[k] = __builtin_fmaf(pi, dv[k], tv[k]);                   // eq. 3
-        if (pi_out) pi_out[k] = pi;
+        tv[k] = __builtin_fmaf(pi[k], dv[k], tv[k]);                // eq. 3
+        if (pi_out) pi_out[k] = pi[k];
     }
     th = make_float4(tv[0], tv[1], tv[2], tv[3]);
     snap = th;
