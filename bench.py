@@ -418,8 +418,10 @@ def main() -> int:
                        if args.pi_hist and variant == "Fast"
                        else "pass_kernel<Generated, %s, diagnostic, depth 2>" % variant
                        if args.pi_hist
+                       # a pass of one commit runs the kernel compiled for one commit
                        else "pass_kernel<Generated, %s, depth %d%s>"
-                       % (variant, depth, ", streaming" if streaming else "")),
+                       % (variant, 1 if wl.K == 1 else depth,
+                          ", streaming" if streaming else "")),
             "copy_ceiling_GBps": copy_gbs,
             "frac_of_copy": achieved / copy_gbs if copy_gbs else None,
             "compute_floor_ms": floor_ms,

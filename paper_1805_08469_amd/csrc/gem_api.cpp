@@ -295,8 +295,11 @@ int run_passes(gem_handle* g, const std::vector<Pass>& passes, Source src,
                          variant == gemk::Variant::Fast;
         // a recording pass loops 8 blocks per compute unit over the groups
         a.rec_grid = rec ? 8 * g->cus : 0;
-        GEM_HIP(gemk::launch_pass(a, src, variant, bf16_out, (g->diag_on || hist) && !rec, rec,
-                                  depth, stream, g->deep_lds, g->stream));
+        const bool diag = (g->diag_on || hist) && !rec;
+        // a single-commit pass runs the kernel compiled for one commit
+        const int d = p.K == 1 && !diag && !rec ? gemk::kPrefetchNone : depth;
+        GEM_HIP(gemk::launch_pass(a, src, variant, bf16_out, diag, rec, d, stream, g->deep_lds,
+                                  g->stream));
         if (g->hist_on) g->hist_count += p.K;
         for (int j = 0; j < p.K; ++j) g->pc[p.worker[j]] = next_pull(g, g->t + j);
         g->t += p.K;

@@ -129,7 +129,9 @@ enum class Variant { General = 0, Fast = 1, FastGlobal = 2 };
 
 // Launchers (defined in gem_kernels.hip).
 // depth: kPrefetchShallow, or kPrefetchDeep for (Generated, Fast, no
-// diagnostics); the routes in a must be planned for the same depth.
+// diagnostics), or kPrefetchNone for a pass of one commit (a.K == 1, no
+// diagnostics, no recording); the routes in a must be planned for the same
+// depth (a single commit's route is the same for every depth).
 // stream_rows: non-temporal row and vector accesses (the diagnostic variant
 // ignores it).  deep_lds: dynamic LDS bytes reserved per block of the
 // deep-ring pass (deep_lds_bytes), 0 for none.

@@ -413,7 +413,8 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
     const uint32_t src = route & kRouteSlotMask;
     const uint32_t dst = (route >> kRouteDstShift) & kRouteSlotMask;
     const int w = a.worker[j];
-    Rows rows = src == kFromRing ? ring : held_get(held, src);
+    // (a single-commit pass reads its one commit's rows through the ring)
+    Rows rows = (DEPTH == 1 || src == kFromRing) ? ring : held_get(held, src);
     constexpr bool FAST = V != Variant::General;
     const bool global_m = V == Variant::FastGlobal ||
                           (V == Variant::General && (a.mode & kModeGlobalProxy));
@@ -507,7 +508,7 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
         __syncthreads();
     }
     if (global_m) ch.mg = r.out.m;
-    if (dst != kToMemory) {
+    if (DEPTH > 1 && dst != kToMemory) {
         // The shared-moment variant carries the moment in ch.mg: a held
         // slot keeps only the snapshot (no registers for a moment copy).
         Rows keep = r.out;
@@ -515,21 +516,22 @@ __device__ __forceinline__ StepOut pass_step(const PassArgs& a, int j, Chunk& ch
         held = held_put(held, dst, keep);
     }
     r.held = held;
+    r.next = ring;
     if (ch.active) {
         // With the shared moment, only snapshot rows move; moment traffic goes
         // to the sink.
         constexpr bool U = V == Variant::FastGlobal;
-        const bool st = dst == kToMemory;
+        const bool st = DEPTH == 1 || dst == kToMemory;
         const bool st_m = st && !global_m;
         row_store<U, NT>(a.S, a.sink_S, st, w, ch, r.out.s);
         row_store<U, NT>(a.M, a.sink_M, st_m, w, ch, r.out.m);
-        const bool pf = (route & kRoutePrefetch) != 0;
-        const int jn = j + DEPTH < a.K ? j + DEPTH : j;
-        const bool pf_m = pf && !global_m;
-        r.next.s = row_load<U, NT>(a.S, a.sink_S, pf, a.worker[jn], ch);
-        r.next.m = row_load<U, NT>(a.M, a.sink_M, pf_m, a.worker[jn], ch);
-    } else {
-        r.next = ring;
+        if constexpr (DEPTH > 1) {
+            const bool pf = (route & kRoutePrefetch) != 0;
+            const int jn = j + DEPTH < a.K ? j + DEPTH : j;
+            const bool pf_m = pf && !global_m;
+            r.next.s = row_load<U, NT>(a.S, a.sink_S, pf, a.worker[jn], ch);
+            r.next.m = row_load<U, NT>(a.M, a.sink_M, pf_m, a.worker[jn], ch);
+        }
     }
     return r;
 }
@@ -570,7 +572,8 @@ __device__ __forceinline__ void pass_group(const PassArgs& a, int64_t grp, uint3
     ch.so = static_cast<uint32_t>(ch.c & a.sink_mask) * 16u;   // = 4 * sink0 + t16
     // The shared moment is worker 0's.
     if (global_m && ch.active) ch.mg = load4_at<NT>(a.M + ch.tile, ch.io);
-    const int K = a.K;
+    // A depth-1 kernel runs single-commit passes only (the launch checks it).
+    const int K = DEPTH == 1 ? 1 : a.K;
     // Ring of prefetched rows, unrolled DEPTH ways so that every entry
     // is a fixed set of registers: commit j reads ring[j mod depth] and refills
     // it for commit j + depth -- no register copy of an in-flight load.
@@ -1227,6 +1230,8 @@ hipError_t launch_one(const PassArgs& a, hipStream_t st, uint32_t lds = 0)
         const uint32_t need = (static_cast<uint32_t>(a.K) * kRecWords + kBlock) * 4u;
         lds = lds > need ? lds : need;
     }
+    static_assert(DEPTH > 1 || (!REC && !DIAG), "depth 1: the plain single-commit pass");
+    if (DEPTH == 1 && a.K != 1) return hipErrorInvalidValue;
     unsigned grid = blocks_for(a.Pp >> 2);
     if (REC && a.rec_grid > 0 && static_cast<unsigned>(a.rec_grid) < grid)
         grid = static_cast<unsigned>(a.rec_grid);
@@ -1273,7 +1278,21 @@ hipError_t launch_fd(const PassArgs& a, Variant v, bool diag, int depth, bool st
         }
         return hipErrorInvalidValue;
     }
-    if (depth != kPrefetchShallow) return hipErrorInvalidValue;
+    if (depth == kPrefetchNone && !diag) {
+        switch (v) {
+        case Variant::Fast:
+            return stream ? launch_one<SRC, Variant::Fast, BF16, false, kPrefetchNone, true>(a, st)
+                          : launch_one<SRC, Variant::Fast, BF16, false, kPrefetchNone, false>(a, st);
+        case Variant::FastGlobal:
+            return stream
+                       ? launch_one<SRC, Variant::FastGlobal, BF16, false, kPrefetchNone, true>(a, st)
+                       : launch_one<SRC, Variant::FastGlobal, BF16, false, kPrefetchNone, false>(a, st);
+        case Variant::General: break;
+        }
+        return stream ? launch_one<SRC, Variant::General, BF16, false, kPrefetchNone, true>(a, st)
+                      : launch_one<SRC, Variant::General, BF16, false, kPrefetchNone, false>(a, st);
+    }
+    if (depth != kPrefetchShallow && depth != kPrefetchNone) return hipErrorInvalidValue;
     switch (v) {
     case Variant::Fast: return launch_d<SRC, Variant::Fast, BF16>(a, diag, stream, st);
     case Variant::FastGlobal: return launch_d<SRC, Variant::FastGlobal, BF16>(a, diag, stream, st);

@@ -21,6 +21,11 @@ constexpr int kHeldSlots = 4;
 constexpr int kPrefetchShallow = 2;
 constexpr int kPrefetchDeep = 4;
 constexpr int kDeepMinK = 16;
+// A pass of one commit needs no ring beyond that commit's own rows and no
+// register slots: its kernel is compiled for exactly one commit (depth 1),
+// which needs fewer registers, so more blocks fit a CU at once -- all of a
+// 1.2M-parameter vector's blocks, instead of a full round and a tail.
+constexpr int kPrefetchNone = 1;
 // Blocks (of 256 threads, one wave per SIMD each) a CU holds at once in the
 // deep-ring pass: measured on MI355X, its row streams run best with 3 waves
 // per SIMD (4 are 1.8% slower, 2 are 7% slower).  The kernel needs few enough

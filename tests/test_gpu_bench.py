@@ -15,9 +15,9 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CASES = [
     (["--pi-hist"], "Fast, recording"),
     (["--pi-hist", "--proxy", "global"], "FastGlobal, diagnostic, depth 2"),
-    (["--cache", "stream"], "streaming"),
+    (["--cache", "stream"], "Fast, depth 1, streaming"),
     (["--pi-scope", "segment"], "seg_step_kernel + seg_blocks_kernel"),
-    (["--proxy", "global", "--cache", "keep"], "FastGlobal"),
+    (["--proxy", "global", "--cache", "keep"], "FastGlobal, depth 1>"),
 ]
 
 

@@ -189,6 +189,11 @@ POLICY_CASES = [
     ("global_proxy", dict(proxy=1), 32, False),
     ("kappa2_linear", dict(kappa=2.0), 32, False),
     ("default_bf16", {}, 16, True),
+    # passes of one commit: the kernels compiled for a single commit
+    ("default_k1", {}, 1, False),
+    ("global_proxy_k1", dict(proxy=1), 1, False),
+    ("kappa2_linear_k1", dict(kappa=2.0), 1, False),
+    ("default_bf16_k1", {}, 1, True),
 ]
 
 
@@ -218,6 +223,28 @@ def test_cache_policies_give_the_same_bits(G, case, mode, K, bf16):
     assert_parity(f"{case} theta", states[G.GEM_CACHE_STREAM][0], st.theta)
     assert_parity(f"{case} S", states[G.GEM_CACHE_STREAM][1], st.S)
     assert_parity(f"{case} M", states[G.GEM_CACHE_STREAM][2], st.M)
+
+
+@pytest.mark.parametrize("mode", [{}, dict(proxy=1)], ids=["default", "global_proxy"])
+def test_single_commit_tail_pass(G, mode):
+    """A run whose last pass holds one commit (T = 2K + 1) switches to the
+    single-commit kernel for it; the state still equals the oracle's."""
+    P, n, K = 8192 + 129, 6, 32
+    T = 2 * K + 1
+    hp = _hp(G, **mode)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=5, pull_mode=hp.pull_mode)
+    from paper_1805_08469_amd.workloads import make_problem
+    h, ts = make_problem(P, 1e-3, 1.0, 5)
+    with G.Gem(P, n, hp) as g:
+        g.set_quadratic(h, ts, 0.01, 0.1, 4)
+        g.sim_run(worker, tau, K)
+        out = (g.theta(), g.S(), g.M(), g.clock)
+    assert out[3] == T
+    st = O.State.initial(n, P)
+    O.run(_ohp(hp, 0.01, 0.1, 4), P, st, np.arange(P), h, ts, worker, tau)
+    assert_parity("theta", out[0], st.theta)
+    assert_parity("S", out[1], st.S)
+    assert_parity("M", out[2], st.M)
 
 
 def test_cache_policy_rejects_unknown_values(G):
