@@ -35,6 +35,12 @@ HBM_PEAK_GBS = 8000.0
 # integer multiplies, transcendental approximations) only lower what a real
 # instruction mix can reach.
 VALU_PEAK_GINST = 256 * 2.4 * 2
+# The same figure counts two lanes' FMAs per packed-FP32 instruction slot; the
+# library builds without packed FP32, and its integer and unpacked instructions
+# issue at one wave64 instruction per SIMD every four cycles: 4 SIMDs x 256 CUs
+# x 2.4 GHz / 4 = 614.4 G/s (the fp64 vector rate, 78.6 TFLOP/s, in the same
+# units).
+VALU_ISSUE_GINST = 256 * 2.4
 METRIC = "parameter-commits/s (P×commits/s) + achieved HBM GB/s vs peak, P=25M n=100"
 KERNEL_SOURCES = ("gem_kernels.hip", "gem_device.hpp", "gem_internal.hpp", "gem_plan.hpp",
                   "gem_layout.hpp")
@@ -375,6 +381,8 @@ def main() -> int:
                 "unit": "G wave64 VALU instructions/s",
                 "frac": ach / VALU_PEAK_GINST if ach else None, "traffic": traffic,
                 "valu_instrs_per_launch": valu,
+                "unpacked_issue_peak": VALU_ISSUE_GINST,
+                "frac_of_unpacked_issue": ach / VALU_ISSUE_GINST if ach else None,
                 "hbm_GBps": achieved, "hbm_frac": achieved / HBM_PEAK_GBS}
     else:
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
