@@ -105,3 +105,54 @@ def test_headline_global_proxy(G):
 
 def test_large(G):
     _workload_parity(G, "large")
+
+
+def test_largest_vector(G):
+    """The largest P the library takes, less 3 (ragged: not a multiple of the
+    16-byte chunk, the 1024-element block or the 8192-element tile), two
+    workers, 33 commits in passes of 32 and 1.  Element indices near 2^31 and
+    table offsets past 2^33 bytes must reach the right elements.  The oracle
+    runs one index per block of the top 2^24 elements, both sides of every
+    tile edge there, the last 16 elements, indices around 2^29 and 2^30 and
+    random indices over the whole vector.  h and theta* repeat a random
+    pattern every 2^20 elements, scaled and shifted per 2^20-element span, so
+    no two spans hold the same values."""
+    P = G.GEM_P_MAX - 3
+    n, T, K = 2, 33, 32
+    need = 4 * P * (2 * n + 3) * 1.05
+    if _free_bytes() < need:
+        pytest.skip(f"needs {need / 2**30:.1f} GiB of device memory")
+    rng = np.random.default_rng(11)
+    span = 1 << 20
+    base_h = np.exp(rng.uniform(np.log(1e-4), 0.0, span)).astype(np.float32)
+    base_t = rng.standard_normal(span).astype(np.float32)
+    h = np.empty(P, dtype=np.float32)
+    ts = np.empty(P, dtype=np.float32)
+    for c in range(-(-P // span)):
+        a, b = c * span, min(P, (c + 1) * span)
+        h[a:b] = base_h[:b - a] * np.float32(1.0 + c * 2.0 ** -12)
+        ts[a:b] = base_t[:b - a] + np.float32(c * 2.0 ** -10)
+    worker, tau = G.gem_schedule_make(n, T, G.GEM_LAW_EXP, seed=3)
+    top = P - (1 << 24)
+    blocks = np.arange(top // BLOCK_ELEMS, -(-P // BLOCK_ELEMS), dtype=np.int64)
+    per_block = blocks * BLOCK_ELEMS + (blocks * 389) % BLOCK_ELEMS
+    edges = np.arange(top // TILE_ELEMS + 1, -(-P // TILE_ELEMS), dtype=np.int64) * TILE_ELEMS
+    fixed = np.array([0, 1, 2, 3, (1 << 29) - 1, 1 << 29, (1 << 30) - 1, 1 << 30,
+                      (1 << 31) - 1024], dtype=np.int64)
+    idx = np.concatenate([fixed, per_block, edges - 1, edges, np.arange(P - 16, P),
+                          rng.integers(0, P, size=20_000)])
+    idx = np.unique(idx[(idx >= 0) & (idx < P)]).astype(np.int64)
+    print(f"[largest] P={P} n={n} T={T} K={K} sample={idx.size}", flush=True)
+    with G.Gem(P, n) as g:
+        g.set_quadratic(h, ts, 0.01, 0.02, 5)
+        g.sim_run(worker, tau, K)
+        theta, S, M = g.gather(idx)
+        stats = g.stats()
+    assert stats.passes == 2 and stats.commits == T
+    hp = O.Hyper(lr=0.01, sigma=0.02, momentum=0.9, seed=5)
+    st = O.State.initial(n, idx.size)
+    O.run(hp, P, st, idx, h[idx], ts[idx], worker, tau)
+    del h, ts
+    assert_parity("largest theta", theta, st.theta)
+    assert_parity("largest S", S, st.S)
+    assert_parity("largest M", M, st.M)
