@@ -86,12 +86,6 @@ __device__ __forceinline__ int scale_bin(float x)
     return 2 + octave * 16 + static_cast<int>((b >> 19) & 0xFu);
 }
 
-// One element of one commit.  th and m are the element's central value and
-// the committing worker's moment (in/out); s is its snapshot; d the update.
-// snap receives the value the worker's snapshot takes after this commit.
-// FAST: the default rule (GEM, CLAMP0, kappa_eff = 1, post-commit pull) with
-// no runtime mode tests; otherwise every mode is read from a.mode.
-// hist_row: the histogram row this element's factor counts in, or null.
 // The default rule's step on a thread's four elements (Fast variants, no
 // diagnostics): the same arithmetic as commit_element, with one range check
 // for the four quotients.  When all eight operand magnitudes lie in
@@ -151,6 +145,12 @@ __device__ __forceinline__ void commit4_fast(const PassArgs& a, const float4& d,
     m = make_float4(mv[0], mv[1], mv[2], mv[3]);
 }
 
+// One element of one commit.  th and m are the element's central value and
+// the committing worker's moment (in/out); s is its snapshot; d the update.
+// snap receives the value the worker's snapshot takes after this commit.
+// FAST: the default rule (GEM, CLAMP0, kappa_eff = 1, post-commit pull) with
+// no runtime mode tests; otherwise every mode is read from a.mode.
+// hist_row: the histogram row this element's factor counts in, or null.
 template <bool FAST, bool DIAG>
 __device__ __forceinline__ void commit_element(const PassArgs& a, int tau, float d, float s,
                                                float& th, float& m, float& snap, bool live,
